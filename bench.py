@@ -1,0 +1,263 @@
+#!/usr/bin/env python3
+"""Benchmark of the W4A4 IE-BME SpMM on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--N n] [--split-k S]
+
+One step is one us_spmm call (stream the IE-BME tiles, decode, multiply,
+combine, store Y and the dequantised Y) over one copy of the encoded weight
+matrix; the encoding itself is offline, as in the paper, and is not timed.
+Every timed round queues its launches behind a bounded spin kernel, so the
+GPU runs them back to back and host launch cost never enters the event
+timings; the weight copies rotate over at least 1 GiB so that none of them
+can be served from the 256 MB Infinity Cache.
+
+Prints one JSON line on stdout; details go to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2608_09291_amd import binding, synth  # noqa: E402
+
+METRIC = "W4A4 SpMM µs/call, achieved HBM GB/s on encoded bytes, dense-equiv TOPS"
+DEFAULT_WORKLOAD = "ffn_down_4096x11008_s50"
+HBM_PEAK_GBS = 8000.0
+ROTATE_BYTES = 1 << 30
+ROUND_LAUNCHES = 200
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--N", type=int, default=0, help="activation columns (default: the workload's first)")
+    ap.add_argument("--split-k", type=int, default=0)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-extras", action="store_true", help="skip the read-ceiling and dense GEMM points")
+    return ap.parse_args()
+
+
+class Timer:
+    """GPU-side timing of back-to-back launches on the current stream."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.stream = torch.cuda.current_stream()
+
+    def run(self, launch, count: int, per_launch_host_us: float = 20.0) -> float:
+        """Total GPU milliseconds of `count` launches (launch(i) enqueues one)."""
+        torch = self.torch
+        total = 0.0
+        done = 0
+        while done < count:
+            n = min(ROUND_LAUNCHES, count - done)
+            # Long enough for the host to queue all n launches before the GPU gets there.
+            binding.probe_spin(int(max(2e6, n * per_launch_host_us * 1e3 * 2)))
+            start = torch.cuda.Event(enable_timing=True)
+            end = torch.cuda.Event(enable_timing=True)
+            start.record(self.stream)
+            for i in range(n):
+                launch(done + i)
+            end.record(self.stream)
+            end.synchronize()
+            total += start.elapsed_time(end)
+            done += n
+        return total
+
+
+def spmm_bench(torch, args, w, N, timer):
+    W = synth.weights(w)
+    Xt = synth.activations(w, N)
+    enc = binding.encode(W)
+    rep = binding.pmr(enc, N)
+    dev0 = binding.to_device(enc)
+    enc_bytes = dev0.nbytes
+    n_copies = max(2, -(-ROTATE_BYTES // enc_bytes))
+    copies = [dev0] + [binding.DeviceEncoded(dev0.bitmaps.clone(), dev0.offsets.clone(),
+                                             dev0.payload.clone(), dev0.M, dev0.K, dev0.n_lt,
+                                             dev0.n_payload) for _ in range(n_copies - 1)]
+    xp = torch.from_numpy(binding.pack_int4(Xt)).cuda()
+    y = torch.empty((N, w.M), dtype=torch.int32, device="cuda")
+    sc = yf = None
+    if w.dequant:
+        sc = torch.from_numpy(synth.scales(w)).cuda()
+        yf = torch.empty((N, w.M), dtype=torch.float32, device="cuda")
+
+    # Prebuilt C arguments: the timed loop only calls the library.
+    L = binding.lib()
+    structs = [c.struct() for c in copies]
+    sptrs = [ctypes.byref(s) for s in structs]
+    opts = binding.SpmmOpts(args.split_k, 0)
+    optp = ctypes.byref(opts)
+    xa, ya = xp.data_ptr(), y.data_ptr()
+    sca = None if sc is None else sc.data_ptr()
+    yfa = None if yf is None else yf.data_ptr()
+    sh = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    status = [0]
+
+    def launch(i):
+        st = L.us_spmm(sptrs[i % n_copies], xa, N, ya, sca, yfa, None, 0, optp, sh)
+        if st:
+            status[0] = st
+
+    timer.run(launch, args.warmup)
+    torch.cuda.synchronize()
+    ms = timer.run(launch, args.steps)
+    if status[0]:
+        raise binding.UsError("us_spmm", status[0])
+
+    # Algorithmic bytes of one call: stored payload (zeros of active groups
+    # included), bitmaps (32 B/LT), offsets (4 B/LT), X, Y, and with the
+    # dequant epilogue the scales and the float32 Y.
+    alg = (rep["payload_stored_bytes"] + rep["bitmap_bytes"] + rep["offset_bytes"]
+           + w.K * N // 2 + w.M * N * 4)
+    if w.dequant:
+        alg += w.M * 4 + w.M * N * 4
+    return dict(W=W, Xt=Xt, enc=enc, rep=rep, ms=ms, alg_bytes=alg, enc_bytes=enc_bytes,
+                n_copies=n_copies, y=y, yf=yf)
+
+
+def read_ceiling(torch, nbytes, steps, timer):
+    """Streaming-read rate of HBM at the same byte count, same rotation."""
+    nbytes = (nbytes + 15) // 16 * 16
+    n_copies = max(2, -(-ROTATE_BYTES // nbytes))
+    bufs = [torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(i % 251) for i in range(n_copies)]
+    sink = torch.empty(binding.probe_read_sink_words(nbytes), dtype=torch.int32, device="cuda")
+    timer.run(lambda i: binding.probe_read(bufs[i % n_copies], nbytes, sink), min(steps, 200))
+    ms = timer.run(lambda i: binding.probe_read(bufs[i % n_copies], nbytes, sink), steps)
+    del bufs
+    return ms / steps
+
+
+def dense_gemm(torch, w, N, steps, timer):
+    """Dense INT8 GEMM of the same shape (1 byte per weight)."""
+    nbytes = w.M * w.K
+    n_copies = max(2, -(-ROTATE_BYTES // nbytes))
+    rng = np.random.default_rng(0)
+    W8 = torch.from_numpy(rng.integers(-128, 128, size=(w.M, w.K), dtype=np.int8)).cuda()
+    mats = [W8] + [W8.clone() for _ in range(n_copies - 1)]
+    x = torch.from_numpy(rng.integers(-128, 128, size=(N, w.K), dtype=np.int8)).cuda()
+    y = torch.empty((N, w.M), dtype=torch.int32, device="cuda")
+    timer.run(lambda i: binding.gemm_i8(mats[i % n_copies], x, w.M, w.K, N, y), min(steps, 200))
+    ms = timer.run(lambda i: binding.gemm_i8(mats[i % n_copies], x, w.M, w.K, N, y), steps)
+    del mats
+    return ms / steps, nbytes + w.K * N + w.M * N * 4
+
+
+def cpu_baseline(w, W, Xt, enc_bytes_alg, budget_s=12.0):
+    """The oracle's int64 masked dense product, timed on this host's cores."""
+    from oracle import iebme, product
+    product.build(force=False)
+    threads = product.max_threads()
+    t0 = time.perf_counter()
+    ref = iebme.encode(W)
+    dense = iebme.decode(ref).astype(np.int8)
+    t_dec = time.perf_counter() - t0
+    times = []
+    t_start = time.perf_counter()
+    while len(times) < 3 or (time.perf_counter() - t_start < budget_s and len(times) < 50):
+        t = time.perf_counter()
+        product.matmul_c(dense, Xt)
+        times.append(time.perf_counter() - t)
+    med = float(np.median(times))
+    return dict(value=round(enc_bytes_alg / med / 1e9, 4), unit="GB/s", cores=threads, kind="oracle",
+                sample=(f"whole {w.M}x{w.K} matrix, N={Xt.shape[0]}: oracle int64 masked dense product "
+                        f"(oracle/matmul_i64.c, OpenMP) over the oracle-decoded weights, median of "
+                        f"{len(times)} calls = {med * 1e3:.1f} ms/call; oracle encode+decode (numpy) "
+                        f"{t_dec:.2f} s, not included"),
+                ms_per_call=round(med * 1e3, 3))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    binding.lib()
+    w = synth.WORKLOADS[args.workload]
+    N = args.N or w.Ns[0]
+    timer = Timer(torch)
+
+    log(f"[bench] workload {w.name} M={w.M} K={w.K} N={N} s={w.sparsity} dequant={w.dequant}")
+    r = spmm_bench(torch, args, w, N, timer)
+    ms_step = r["ms"] / args.steps
+    us = ms_step * 1e3
+    gbs = r["alg_bytes"] / (ms_step * 1e-3) / 1e9
+    tops = 2.0 * w.M * w.K * N / (ms_step * 1e-3) / 1e12
+    log(f"[bench] us_spmm {us:.3f} us/call  {gbs:.1f} GB/s on {r['alg_bytes'] / 1e6:.2f} MB  "
+        f"{tops:.1f} dense-equiv TOPS  ({r['n_copies']} rotating copies)")
+
+    extras = {}
+    if not args.no_extras:
+        ceil_ms = read_ceiling(torch, r["alg_bytes"], min(args.steps, 1000), timer)
+        extras["read_ceiling_gbs"] = round(r["alg_bytes"] / (ceil_ms * 1e-3) / 1e9, 1)
+        extras["read_ceiling_us"] = round(ceil_ms * 1e3, 3)
+        g_ms, g_bytes = dense_gemm(torch, w, N, min(args.steps, 1000), timer)
+        extras["dense_int8_gemm_us"] = round(g_ms * 1e3, 3)
+        extras["dense_int8_gemm_gbs"] = round(g_bytes / (g_ms * 1e-3) / 1e9, 1)
+        extras["speedup_vs_dense_int8"] = round(g_ms / ms_step, 3)
+        log(f"[bench] read ceiling {extras['read_ceiling_us']} us ({extras['read_ceiling_gbs']} GB/s); "
+            f"dense int8 GEMM {extras['dense_int8_gemm_us']} us")
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(w, r["W"], r["Xt"], r["alg_bytes"])
+        log(f"[bench] cpu oracle {cpu['ms_per_call']} ms/call on {cpu['cores']} threads")
+
+    rep = r["rep"]
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": w.name, "M": w.M, "K": w.K, "N": N, "sparsity": w.sparsity,
+                   "dequant": w.dequant, "split_k": args.split_k or "auto",
+                   "weights": "w4a4 IE-BME (16x64 tiles, 2x2 areas), int8 MFMA, int32 accumulate",
+                   "rotating_copies": r["n_copies"]},
+        "us_per_call": round(us, 3),
+        "dense_equiv_tops": round(tops, 2),
+        "encoded_mb": round(r["alg_bytes"] / 1e6, 3),
+        "pmr": round(rep["pmr"], 4),
+        "pmr_stored": round(rep["pmr_stored"], 4),
+        "ci_eff_eq2": round(rep["ci_eff"], 3),
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "us_spmm_kernel",
+                     "bytes_per_launch": r["alg_bytes"]},
+        "cpu_baseline": cpu,
+        **extras,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,179 @@
+/*
+ * us.h - C-ABI of the UnionSparse W4A4 IE-BME SpMM library for MI355X (gfx950).
+ *
+ * The library encodes a masked INT4 weight matrix into the paper's
+ * Index-Efficient Bitmap Encoding (IE-BME, Section V-A), multiplies it on the
+ * GPU by dense INT4 activations into INT32 (the kernel of Section VI,
+ * "UnionSparse Kernel" algorithm), and accounts its bytes by the
+ * Payload-to-Metadata Ratio (Eq. 1) and effective compute intensity (Eq. 2).
+ *
+ * Conventions for every call:
+ *   - arguments are checked before any work; a negative us_status means
+ *     nothing was written and nothing was launched;
+ *   - device pointers are plain HIP device addresses owned by the caller;
+ *   - a stream argument is a hipStream_t passed as void * (NULL = the null
+ *     stream); GPU calls are asynchronous on that stream, never synchronise
+ *     and never allocate device memory;
+ *   - the library keeps no global state and is thread-safe.
+ */
+#ifndef UNIONSPARSE_US_H
+#define UNIONSPARSE_US_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    US_OK = 0,
+    US_ERR_ARG = -1,     /* null pointer, bad option value, misaligned pointer */
+    US_ERR_SHAPE = -2,   /* M % 16, K % 64, N outside [1, 32], size limits */
+    US_ERR_RANGE = -3,   /* a weight outside the signed INT4 range [-8, 7] */
+    US_ERR_NOMEM = -4,   /* host allocation failed (encoder only) */
+    US_ERR_DEVICE = -5,  /* the HIP launch reported an error */
+    US_ERR_FORMAT = -6   /* encoded arrays are inconsistent with each other */
+} us_status;
+
+/* Fixed IE-BME geometry of the hot path (Section V-A; the LT size is given in
+ * the caption of the encoding figure, R_A = C_A = 2 in every illustration). */
+#define US_LT_H 16          /* H_L: rows of a local tile (LT)              */
+#define US_LT_W 64          /* K_L: columns of an LT                       */
+#define US_RA 2             /* R_A: area rows per LT                       */
+#define US_CA 2             /* C_A: area columns per LT (Q = R_A C_A = 4)  */
+#define US_WORDS_PER_LT 4   /* 8 x 32 union-mask bits = four 64-bit words  */
+#define US_PAYLOAD_PAD 16   /* zero bytes after the payload                */
+#define US_N_MAX 32         /* widest activation matrix                    */
+#define US_K_MAX 130048     /* K bound: int32 headroom of the kernel's scaled sums */
+
+/*
+ * Host IE-BME matrix (Section V-A, "IE-BME Storage Layout").
+ *
+ * LT t = mb * (K/64) + kb covers rows [16 mb, 16 mb + 16) and columns
+ * [64 kb, 64 kb + 64). Area q = a * 2 + c holds LT rows [8a, 8a + 8) and
+ * columns [32c, 32c + 32). Union-mask bit (i, j), i < 8, j < 32, is set when
+ * any area is nonzero at (i, j); it is bit (32 i + j) % 64 of word
+ * 4 t + (32 i + j) / 64 of `bitmaps`. offsets[t] = sum over tau < t of 4 P_tau
+ * (P = active union-mask bits), in INT4 values, with offsets[n_lt] the total.
+ * Payload value o_t + q P_t + rho (rho = rank of (i, j) among active bits,
+ * row-major) is area q's value at (i, j); value n is the low nibble of byte
+ * n / 2 when n is even, the high nibble when odd, in two's complement.
+ *
+ * The three arrays are allocated by us_encode and freed by us_iebme_free.
+ */
+typedef struct {
+    int32_t M, K;                 /* weight matrix is M x K                 */
+    int32_t lt_h, lt_w, ra, ca;   /* 16, 64, 2, 2                           */
+    int64_t n_lt;                 /* (M/16) * (K/64)                        */
+    int64_t nnz;                  /* nonzero weights                        */
+    int64_t n_payload;            /* stored INT4 values = offsets[n_lt]     */
+    int64_t payload_bytes;        /* ceil(n_payload / 2) + US_PAYLOAD_PAD   */
+    uint64_t *bitmaps;            /* n_lt * 4 words                         */
+    uint32_t *offsets;            /* n_lt + 1 entries                       */
+    uint8_t *payload;             /* payload_bytes bytes, zeroed padding    */
+} us_iebme;
+
+/*
+ * us_encode - IE-BME encoding of a masked INT4 matrix (Section V-A: area
+ * partitioning, shared union mask, the three storage arrays).
+ *   w    : host int8, M rows of `ldw` elements, values in [-8, 7], 0 = pruned
+ *   M, K : M % 16 == 0, K % 64 == 0, M * K < 2^32
+ *   ldw  : row stride of w in elements, >= K
+ *   out  : filled on success; on error it is left untouched
+ * Returns US_ERR_ARG, US_ERR_SHAPE, US_ERR_RANGE or US_ERR_NOMEM on failure.
+ */
+us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out);
+
+/* us_iebme_free - release the arrays of an encoded matrix and zero it. */
+void us_iebme_free(us_iebme *m);
+
+/*
+ * Byte accounting of an encoded matrix (Section III-B, Eq. 1; Section III-C,
+ * Eq. 2). Metadata is bitmaps (32 B per LT) plus offsets (4 B per LT; the
+ * sentinel is not counted). B_w = 1/2 byte for INT4.
+ */
+typedef struct {
+    int64_t nnz;                  /* nonzero weights                           */
+    int64_t stored_values;        /* n_payload: nnz plus zeros of active groups */
+    int64_t n_lt;
+    int64_t payload_stored_bytes; /* ceil(stored_values / 2)                   */
+    int64_t bitmap_bytes;         /* 32 n_lt                                   */
+    int64_t offset_bytes;         /* 4 n_lt                                    */
+    int64_t meta_bytes;           /* Stor_meta of Eq. 1                        */
+    double payload_useful_bytes;  /* B_w * nnz                                 */
+    double pmr;                   /* Eq. 1: payload_useful_bytes / meta_bytes  */
+    double pmr_stored;            /* stored payload bytes / meta_bytes         */
+    double ci_eff;                /* Eq. 2 for activation width N, as printed  */
+} us_pmr_report;
+
+/*
+ * us_pmr - fill `out` for `m`; N > 0 also evaluates Eq. 2 (N = 0 leaves
+ * ci_eff at 0). Checks that offsets agree with the bitmaps (US_ERR_FORMAT).
+ */
+us_status us_pmr(const us_iebme *m, int32_t N, us_pmr_report *out);
+
+/* An IE-BME matrix whose three arrays the caller has copied to the GPU. */
+typedef struct {
+    const uint64_t *bitmaps;      /* device, n_lt * 4 words, 8-byte aligned  */
+    const uint32_t *offsets;      /* device, n_lt + 1 entries, 4-byte aligned */
+    const uint8_t *payload;       /* device, ceil(n_payload / 2) + US_PAYLOAD_PAD bytes */
+    int32_t M, K;
+    int64_t n_lt, n_payload;
+} us_iebme_dev;
+
+typedef struct {
+    int32_t split_k;  /* K slices per 16-row block, one wavefront each:
+                         0 = automatic, else 1, 2, 4, 8 or 16            */
+    int32_t variant;  /* reserved, must be 0                             */
+} us_spmm_opts;
+
+/*
+ * us_spmm_workspace_size - device workspace bytes us_spmm needs for this
+ * shape and options (0 today: the split-K sums are combined on chip).
+ */
+us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, const us_spmm_opts *opts,
+                                 size_t *bytes);
+
+/*
+ * us_spmm - Y = W X on the GPU: W in IE-BME (device copy), X dense INT4,
+ * INT32 accumulation (Section VI, "UnionSparse Kernel" algorithm: the kernel
+ * takes the IE-BME matrix, the activations and a split-K count, and returns Y).
+ *   w      : encoded matrix, device arrays
+ *   x      : device, N x K row-major INT4, two values per byte along K
+ *            (even k in the low nibble), 4-byte aligned
+ *   N      : 1..32 activation columns
+ *   y      : device int32, N x M row-major (y[n * M + m] = Y[m][n])
+ *   scale  : device float32[M] or NULL; with it, y_f32[n * M + m] =
+ *            fl32(fl32(Y[m][n]) * scale[m]) is written too (the dequant
+ *            epilogue is not part of the paper)
+ *   y_f32  : device float32, N x M row-major; NULL exactly when scale is NULL
+ *   ws     : device workspace of ws_bytes (may be NULL when the size is 0)
+ *   opts   : NULL for automatic choices
+ *   stream : hipStream_t
+ * Argument errors return before launch; a launch error returns US_ERR_DEVICE.
+ */
+us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N, int32_t *y,
+                  const float *scale, float *y_f32, void *ws, size_t ws_bytes,
+                  const us_spmm_opts *opts, void *stream);
+
+/*
+ * us_gemm_i8 - dense INT8 GEMM, Y = W X with INT32 accumulation, on the int8
+ * matrix cores: the in-library dense comparison point (the paper compares
+ * against dense Tensor-Core GEMMs, Section VII-A "Baselines and Fairness").
+ *   w : device int8, M x K row-major, 16-byte aligned
+ *   x : device int8, N x K row-major (row n is activation column n), 16-byte aligned
+ *   y : device int32, N x M row-major
+ * M % 16 == 0, K % 64 == 0, K <= US_K_MAX, 1 <= N <= 32.
+ */
+us_status us_gemm_i8(const int8_t *w, const int8_t *x, int32_t M, int32_t K, int32_t N,
+                     int32_t *y, void *stream);
+
+/* us_status_string - static text naming a status code. */
+const char *us_status_string(us_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UNIONSPARSE_US_H */

@@ -1,0 +1,265 @@
+"""Python binding of the UnionSparse C-ABI (include/us.h, include/us_probe.h).
+
+Argument marshalling only: every computation happens in the native library
+(the encoder in C++, the products in HIP kernels). PyTorch provides device
+memory and streams. The library must have been built in-tree
+(``python -m paper_2608_09291_amd.build``); without it every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libunionsparse.so")
+
+US_OK = 0
+STATUS = {0: "US_OK", -1: "US_ERR_ARG", -2: "US_ERR_SHAPE", -3: "US_ERR_RANGE",
+          -4: "US_ERR_NOMEM", -5: "US_ERR_DEVICE", -6: "US_ERR_FORMAT"}
+PAYLOAD_PAD = 16
+N_MAX = 32
+K_MAX = 130048
+
+#: Every symbol the two public headers declare.
+EXPORTS = ("us_encode", "us_iebme_free", "us_pmr", "us_spmm_workspace_size", "us_spmm",
+           "us_gemm_i8", "us_status_string", "us_probe_read", "us_probe_read_sink_words",
+           "us_probe_copy", "us_probe_spin")
+
+
+class UsError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {STATUS.get(status, status)}")
+        self.status = status
+
+
+class IEBME(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int32), ("K", ctypes.c_int32),
+                ("lt_h", ctypes.c_int32), ("lt_w", ctypes.c_int32),
+                ("ra", ctypes.c_int32), ("ca", ctypes.c_int32),
+                ("n_lt", ctypes.c_int64), ("nnz", ctypes.c_int64),
+                ("n_payload", ctypes.c_int64), ("payload_bytes", ctypes.c_int64),
+                ("bitmaps", ctypes.POINTER(ctypes.c_uint64)),
+                ("offsets", ctypes.POINTER(ctypes.c_uint32)),
+                ("payload", ctypes.POINTER(ctypes.c_uint8))]
+
+
+class PMRReport(ctypes.Structure):
+    _fields_ = [("nnz", ctypes.c_int64), ("stored_values", ctypes.c_int64),
+                ("n_lt", ctypes.c_int64), ("payload_stored_bytes", ctypes.c_int64),
+                ("bitmap_bytes", ctypes.c_int64), ("offset_bytes", ctypes.c_int64),
+                ("meta_bytes", ctypes.c_int64), ("payload_useful_bytes", ctypes.c_double),
+                ("pmr", ctypes.c_double), ("pmr_stored", ctypes.c_double),
+                ("ci_eff", ctypes.c_double)]
+
+
+class IEBMEDev(ctypes.Structure):
+    _fields_ = [("bitmaps", ctypes.c_void_p), ("offsets", ctypes.c_void_p),
+                ("payload", ctypes.c_void_p), ("M", ctypes.c_int32), ("K", ctypes.c_int32),
+                ("n_lt", ctypes.c_int64), ("n_payload", ctypes.c_int64)]
+
+
+class SpmmOpts(ctypes.Structure):
+    _fields_ = [("split_k", ctypes.c_int32), ("variant", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load the native library (once); raise if it was not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run `python -m paper_2608_09291_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        L.us_encode.argtypes = [vp, i32, i32, i64, ctypes.POINTER(IEBME)]
+        L.us_iebme_free.argtypes = [ctypes.POINTER(IEBME)]
+        L.us_iebme_free.restype = None
+        L.us_pmr.argtypes = [ctypes.POINTER(IEBME), i32, ctypes.POINTER(PMRReport)]
+        L.us_spmm_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(SpmmOpts),
+                                             ctypes.POINTER(sz)]
+        L.us_spmm.argtypes = [ctypes.POINTER(IEBMEDev), vp, i32, vp, vp, vp, vp, sz,
+                              ctypes.POINTER(SpmmOpts), vp]
+        L.us_gemm_i8.argtypes = [vp, vp, i32, i32, i32, vp, vp]
+        L.us_status_string.argtypes = [ctypes.c_int]
+        L.us_status_string.restype = ctypes.c_char_p
+        L.us_probe_read.argtypes = [vp, sz, vp, vp]
+        L.us_probe_read_sink_words.argtypes = [sz]
+        L.us_probe_read_sink_words.restype = sz
+        L.us_probe_copy.argtypes = [vp, vp, sz, vp]
+        L.us_probe_spin.argtypes = [ctypes.c_uint64, vp]
+        for name in ("us_encode", "us_pmr", "us_spmm_workspace_size", "us_spmm", "us_gemm_i8",
+                     "us_probe_read", "us_probe_copy", "us_probe_spin"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(fn: str, status: int):
+    if status != US_OK:
+        raise UsError(fn, status)
+
+
+# ---------------------------------------------------------------------------
+# Host encoder and byte accounting
+# ---------------------------------------------------------------------------
+
+class Encoded:
+    """An IE-BME matrix produced by us_encode; owns the native arrays."""
+
+    def __init__(self, s: IEBME):
+        self._s = s
+
+    @property
+    def M(self): return self._s.M
+
+    @property
+    def K(self): return self._s.K
+
+    @property
+    def n_lt(self): return self._s.n_lt
+
+    @property
+    def nnz(self): return self._s.nnz
+
+    @property
+    def n_payload(self): return self._s.n_payload
+
+    @property
+    def bitmaps(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self._s.bitmaps, shape=(4 * self._s.n_lt,))
+
+    @property
+    def offsets(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self._s.offsets, shape=(self._s.n_lt + 1,))
+
+    @property
+    def payload(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self._s.payload, shape=(self._s.payload_bytes,))
+
+    def struct(self) -> IEBME:
+        return self._s
+
+    def free(self):
+        if self._s is not None and self._s.bitmaps:
+            lib().us_iebme_free(ctypes.byref(self._s))
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def encode(W: np.ndarray) -> Encoded:
+    """us_encode on a host int8 matrix (values in [-8, 7])."""
+    W = np.ascontiguousarray(W, dtype=np.int8)
+    if W.ndim != 2:
+        raise ValueError("W must be 2-D")
+    s = IEBME()
+    _check("us_encode", lib().us_encode(W.ctypes.data, W.shape[0], W.shape[1], W.shape[1],
+                                        ctypes.byref(s)))
+    return Encoded(s)
+
+
+def pmr(enc: Encoded, N: int = 0) -> dict:
+    r = PMRReport()
+    _check("us_pmr", lib().us_pmr(ctypes.byref(enc.struct()), N, ctypes.byref(r)))
+    return {name: getattr(r, name) for name, _ in PMRReport._fields_}
+
+
+# ---------------------------------------------------------------------------
+# Device side
+# ---------------------------------------------------------------------------
+
+def _stream_handle(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+@dataclass
+class DeviceEncoded:
+    """Device copies of the three IE-BME arrays (torch tensors) and the C struct."""
+
+    bitmaps: "object"
+    offsets: "object"
+    payload: "object"
+    M: int
+    K: int
+    n_lt: int
+    n_payload: int
+
+    def struct(self) -> IEBMEDev:
+        return IEBMEDev(self.bitmaps.data_ptr(), self.offsets.data_ptr(), self.payload.data_ptr(),
+                        self.M, self.K, self.n_lt, self.n_payload)
+
+    @property
+    def nbytes(self) -> int:
+        """Encoded bytes the kernel streams: bitmaps, offsets and stored payload."""
+        return 32 * self.n_lt + 4 * (self.n_lt + 1) + (self.n_payload + 1) // 2
+
+
+def to_device(enc: Encoded, device="cuda") -> DeviceEncoded:
+    import torch
+    bm = torch.from_numpy(enc.bitmaps.view(np.int64).copy()).to(device)
+    off = torch.from_numpy(enc.offsets.view(np.int32).copy()).to(device)
+    pay = torch.from_numpy(enc.payload.copy()).to(device)
+    return DeviceEncoded(bm, off, pay, enc.M, enc.K, enc.n_lt, enc.n_payload)
+
+
+def pack_int4(Xt: np.ndarray) -> np.ndarray:
+    """(N, K) int8 INT4 values -> (N, K/2) bytes, even k in the low nibble."""
+    Xt = np.asarray(Xt, dtype=np.int8)
+    u = (Xt.astype(np.int16) & 0xF).astype(np.uint8)
+    return np.ascontiguousarray(u[:, 0::2] | (u[:, 1::2] << 4))
+
+
+def workspace_size(M: int, K: int, N: int, split_k: int = 0) -> int:
+    n = ctypes.c_size_t(0)
+    opts = SpmmOpts(split_k, 0)
+    _check("us_spmm_workspace_size",
+           lib().us_spmm_workspace_size(M, K, N, ctypes.byref(opts), ctypes.byref(n)))
+    return n.value
+
+
+def spmm(w: DeviceEncoded, x_packed, N: int, y, scale=None, y_f32=None, split_k: int = 0,
+         ws=None, stream=None, wstruct: IEBMEDev = None) -> None:
+    """us_spmm: y[n, m] = sum_k W[m, k] X[k, n] (+ optional dequant into y_f32)."""
+    s = wstruct if wstruct is not None else w.struct()
+    opts = SpmmOpts(split_k, 0)
+    _check("us_spmm", lib().us_spmm(
+        ctypes.byref(s), x_packed.data_ptr(), N, y.data_ptr(),
+        None if scale is None else scale.data_ptr(),
+        None if y_f32 is None else y_f32.data_ptr(),
+        None if ws is None else ws.data_ptr(), 0 if ws is None else ws.numel() * ws.element_size(),
+        ctypes.byref(opts), _stream_handle(stream)))
+
+
+def gemm_i8(w, x, M: int, K: int, N: int, y, stream=None) -> None:
+    """us_gemm_i8: dense int8 (M, K) times int8 (N, K)^T into int32 (N, M)."""
+    _check("us_gemm_i8", lib().us_gemm_i8(w.data_ptr(), x.data_ptr(), M, K, N, y.data_ptr(),
+                                          _stream_handle(stream)))
+
+
+def probe_read(src, nbytes: int, sink, stream=None) -> None:
+    _check("us_probe_read", lib().us_probe_read(src.data_ptr(), nbytes, sink.data_ptr(),
+                                                _stream_handle(stream)))
+
+
+def probe_read_sink_words(nbytes: int) -> int:
+    return int(lib().us_probe_read_sink_words(nbytes))
+
+
+def probe_copy(src, dst, nbytes: int, stream=None) -> None:
+    _check("us_probe_copy", lib().us_probe_copy(src.data_ptr(), dst.data_ptr(), nbytes,
+                                                _stream_handle(stream)))
+
+
+def probe_spin(ns: int, stream=None) -> None:
+    _check("us_probe_spin", lib().us_probe_spin(int(ns), _stream_handle(stream)))

@@ -1,0 +1,72 @@
+"""Build the UnionSparse shared library in-tree for gfx950.
+
+    python -m paper_2608_09291_amd.build
+
+compiles ``csrc/*.hip`` with hipcc (gfx950 only, packed FP32 instructions
+disabled) and ``csrc/*.cpp`` with g++, and links ``libunionsparse.so`` next to
+this file.
+"""
+from __future__ import annotations
+
+import concurrent.futures as cf
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+BUILD = os.path.join(PKG, "_build")
+LIB = os.path.join(PKG, "libunionsparse.so")
+
+ARCH = "gfx950"
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-fno-strict-aliasing",
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-I", INCLUDE]
+CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-fno-strict-aliasing", "-Wall", "-I", INCLUDE]
+
+
+def _sources():
+    hip = sorted(f for f in os.listdir(CSRC) if f.endswith(".hip"))
+    cpp = sorted(f for f in os.listdir(CSRC) if f.endswith(".cpp"))
+    return hip, cpp
+
+
+def _compile(cmd):
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("compile failed:\n" + " ".join(cmd) + "\n" + r.stdout + r.stderr)
+    return r.stderr
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source and link the library; returns its path."""
+    os.makedirs(BUILD, exist_ok=True)
+    hip, cpp = _sources()
+    jobs = []
+    for f in hip:
+        obj = os.path.join(BUILD, f + ".o")
+        jobs.append((obj, [HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, f), "-o", obj]))
+    for f in cpp:
+        obj = os.path.join(BUILD, f + ".o")
+        jobs.append((obj, ["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, f), "-o", obj]))
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
+        logs = list(ex.map(lambda j: _compile(j[1]), jobs))
+    if verbose:
+        for (obj, cmd), log in zip(jobs, logs):
+            print(" ".join(cmd))
+    tmp = LIB + ".tmp"
+    _compile([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *[o for o, _ in jobs],
+              "-o", tmp, "-lpthread"])
+    os.replace(tmp, LIB)
+    return LIB
+
+
+def clean():
+    shutil.rmtree(BUILD, ignore_errors=True)
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

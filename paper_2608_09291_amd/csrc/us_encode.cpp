@@ -1,0 +1,227 @@
+// Host side of the IE-BME format: encoder (Section V-A) and byte accounting
+// (Eq. 1, Eq. 2). Runs offline on the CPU, as the paper's format conversion
+// does; its cost is not part of the SpMM latency.
+#include <algorithm>
+#include <atomic>
+#include <cstdlib>
+#include <cstring>
+#include <thread>
+#include <vector>
+
+#include "us.h"
+
+namespace {
+
+constexpr int kAreaH = US_LT_H / US_RA;   // 8 union-mask rows
+constexpr int kAreaW = US_LT_W / US_CA;   // 32 union-mask columns
+
+// Run body(lo, hi) over [0, n) on up to hardware_concurrency threads.
+template <typename F>
+void parallel_ranges(int64_t n, F body) {
+    unsigned hw = std::thread::hardware_concurrency();
+    int64_t nt = std::max<int64_t>(1, std::min<int64_t>(hw ? hw : 1, (n + 1023) / 1024));
+    if (nt == 1) {
+        body(int64_t(0), n);
+        return;
+    }
+    std::vector<std::thread> th;
+    th.reserve(nt);
+    for (int64_t t = 0; t < nt; ++t)
+        th.emplace_back([=] { body(n * t / nt, n * (t + 1) / nt); });
+    for (auto &x : th) x.join();
+}
+
+inline int popcount64(uint64_t v) { return __builtin_popcountll(v); }
+
+// Value of area q at union-mask position (i, j) of the LT whose top-left
+// element is `base`: area q = a * C_A + c covers LT rows [8a, 8a+8) and
+// columns [32c, 32c+32).
+inline int8_t area_value(const int8_t *base, int64_t ldw, int q, int i, int j) {
+    const int a = q / US_CA, c = q % US_CA;
+    return base[(int64_t)(a * kAreaH + i) * ldw + c * kAreaW + j];
+}
+
+}  // namespace
+
+extern "C" const char *us_status_string(us_status s) {
+    switch (s) {
+        case US_OK: return "ok";
+        case US_ERR_ARG: return "invalid argument";
+        case US_ERR_SHAPE: return "unsupported shape";
+        case US_ERR_RANGE: return "weight outside INT4 range";
+        case US_ERR_NOMEM: return "out of host memory";
+        case US_ERR_DEVICE: return "HIP launch error";
+        case US_ERR_FORMAT: return "inconsistent IE-BME arrays";
+    }
+    return "unknown status";
+}
+
+extern "C" us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out) {
+    if (!w || !out) return US_ERR_ARG;
+    if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W) return US_ERR_SHAPE;
+    if (ldw < K) return US_ERR_ARG;
+    if ((uint64_t)M * (uint64_t)K >= (1ull << 32)) return US_ERR_SHAPE;
+
+    // Every weight must be a signed INT4 value.
+    std::atomic<bool> bad{false};
+    parallel_ranges(M, [&](int64_t r0, int64_t r1) {
+        for (int64_t r = r0; r < r1 && !bad.load(std::memory_order_relaxed); ++r) {
+            const int8_t *row = w + r * ldw;
+            for (int32_t k = 0; k < K; ++k)
+                if (row[k] < -8 || row[k] > 7) { bad = true; break; }
+        }
+    });
+    if (bad) return US_ERR_RANGE;
+
+    const int64_t nkb = K / US_LT_W;
+    const int64_t n_lt = (int64_t)(M / US_LT_H) * nkb;
+    uint64_t *bitmaps = (uint64_t *)std::calloc((size_t)n_lt * US_WORDS_PER_LT, sizeof(uint64_t));
+    uint32_t *offsets = (uint32_t *)std::calloc((size_t)n_lt + 1, sizeof(uint32_t));
+    std::vector<uint32_t> P;
+    std::vector<int64_t> nnz_part;
+    try {
+        P.resize((size_t)n_lt);
+    } catch (...) {
+        std::free(bitmaps);
+        std::free(offsets);
+        return US_ERR_NOMEM;
+    }
+    if (!bitmaps || !offsets) {
+        std::free(bitmaps);
+        std::free(offsets);
+        return US_ERR_NOMEM;
+    }
+
+    // Pass 1: shared union mask B_t and P_t = ||B_t||_0 per LT; count nonzeros.
+    std::atomic<int64_t> nnz{0};
+    parallel_ranges(n_lt, [&](int64_t t0, int64_t t1) {
+        int64_t local_nnz = 0;
+        for (int64_t t = t0; t < t1; ++t) {
+            const int8_t *base = w + (t / nkb) * US_LT_H * ldw + (t % nkb) * US_LT_W;
+            uint64_t *bm = bitmaps + t * US_WORDS_PER_LT;
+            uint32_t p = 0;
+            for (int i = 0; i < kAreaH; ++i) {
+                for (int j = 0; j < kAreaW; ++j) {
+                    bool any = false;
+                    for (int q = 0; q < US_RA * US_CA; ++q) {
+                        const bool nz = area_value(base, ldw, q, i, j) != 0;
+                        local_nnz += nz;
+                        any |= nz;
+                    }
+                    if (any) {
+                        const int L = i * kAreaW + j;   // row-major, leftmost = LSB
+                        bm[L >> 6] |= 1ull << (L & 63);
+                        ++p;
+                    }
+                }
+            }
+            P[(size_t)t] = p;
+        }
+        nnz += local_nnz;
+    });
+
+    // Union Value Offsets: o_t = sum over earlier LTs of Q * P_tau.
+    uint64_t run = 0;
+    for (int64_t t = 0; t < n_lt; ++t) {
+        offsets[t] = (uint32_t)run;
+        run += (uint64_t)(US_RA * US_CA) * P[(size_t)t];
+    }
+    offsets[n_lt] = (uint32_t)run;   // run <= M * K < 2^32
+
+    const int64_t payload_bytes = (int64_t)((run + 1) / 2) + US_PAYLOAD_PAD;
+    uint8_t *payload = (uint8_t *)std::calloc((size_t)payload_bytes, 1);
+    if (!payload) {
+        std::free(bitmaps);
+        std::free(offsets);
+        return US_ERR_NOMEM;
+    }
+
+    // Pass 2: Compressed Values, CV[o_t + q P_t + rho] = W_t^(q)(i, j) for
+    // every active (i, j), zeros of active groups included. Each LT starts on
+    // a multiple of four values, so LTs never share a byte.
+    parallel_ranges(n_lt, [&](int64_t t0, int64_t t1) {
+        for (int64_t t = t0; t < t1; ++t) {
+            const int8_t *base = w + (t / nkb) * US_LT_H * ldw + (t % nkb) * US_LT_W;
+            const uint64_t *bm = bitmaps + t * US_WORDS_PER_LT;
+            const uint64_t o = offsets[t];
+            const uint64_t Pt = P[(size_t)t];
+            uint64_t rho = 0;
+            for (int L = 0; L < kAreaH * kAreaW; ++L) {
+                if (!((bm[L >> 6] >> (L & 63)) & 1)) continue;
+                const int i = L / kAreaW, j = L % kAreaW;
+                for (int q = 0; q < US_RA * US_CA; ++q) {
+                    const uint64_t n = o + (uint64_t)q * Pt + rho;
+                    const uint8_t nib = (uint8_t)area_value(base, ldw, q, i, j) & 0xF;
+                    payload[n >> 1] |= (uint8_t)(nib << ((n & 1) * 4));
+                }
+                ++rho;
+            }
+        }
+    });
+
+    out->M = M;
+    out->K = K;
+    out->lt_h = US_LT_H;
+    out->lt_w = US_LT_W;
+    out->ra = US_RA;
+    out->ca = US_CA;
+    out->n_lt = n_lt;
+    out->nnz = nnz.load();
+    out->n_payload = (int64_t)run;
+    out->payload_bytes = payload_bytes;
+    out->bitmaps = bitmaps;
+    out->offsets = offsets;
+    out->payload = payload;
+    return US_OK;
+}
+
+extern "C" void us_iebme_free(us_iebme *m) {
+    if (!m) return;
+    std::free(m->bitmaps);
+    std::free(m->offsets);
+    std::free(m->payload);
+    std::memset(m, 0, sizeof(*m));
+}
+
+extern "C" us_status us_pmr(const us_iebme *m, int32_t N, us_pmr_report *out) {
+    if (!m || !out || !m->bitmaps || !m->offsets) return US_ERR_ARG;
+    if (N < 0) return US_ERR_ARG;
+    if (m->M <= 0 || m->K <= 0 || m->M % US_LT_H || m->K % US_LT_W) return US_ERR_SHAPE;
+    if (m->lt_h != US_LT_H || m->lt_w != US_LT_W || m->ra != US_RA || m->ca != US_CA)
+        return US_ERR_FORMAT;
+    const int64_t n_lt = (int64_t)(m->M / US_LT_H) * (m->K / US_LT_W);
+    if (m->n_lt != n_lt) return US_ERR_FORMAT;
+
+    // offsets[t + 1] - offsets[t] must be Q times the LT's union-mask popcount.
+    if (m->offsets[0] != 0) return US_ERR_FORMAT;
+    for (int64_t t = 0; t < n_lt; ++t) {
+        int p = 0;
+        for (int k = 0; k < US_WORDS_PER_LT; ++k) p += popcount64(m->bitmaps[t * US_WORDS_PER_LT + k]);
+        if ((uint64_t)m->offsets[t + 1] != (uint64_t)m->offsets[t] + (uint64_t)(US_RA * US_CA) * p)
+            return US_ERR_FORMAT;
+    }
+    if ((int64_t)m->offsets[n_lt] != m->n_payload) return US_ERR_FORMAT;
+    if (m->nnz < 0 || m->nnz > m->n_payload) return US_ERR_FORMAT;
+
+    const double bw = 0.5;   // bytes per INT4 weight
+    us_pmr_report r;
+    std::memset(&r, 0, sizeof(r));
+    r.nnz = m->nnz;
+    r.stored_values = m->n_payload;
+    r.n_lt = n_lt;
+    r.payload_stored_bytes = (m->n_payload + 1) / 2;
+    r.bitmap_bytes = 8 * US_WORDS_PER_LT * n_lt;
+    r.offset_bytes = 4 * n_lt;
+    r.meta_bytes = r.bitmap_bytes + r.offset_bytes;
+    r.payload_useful_bytes = bw * (double)m->nnz;
+    r.pmr = r.payload_useful_bytes / (double)r.meta_bytes;
+    r.pmr_stored = bw * (double)m->n_payload / (double)r.meta_bytes;
+    if (N > 0 && m->nnz > 0) {
+        // Eq. 2 as printed: 2 M N (1-s) / (B_w M (1-s)(1 + 1/PMR) + B_w N).
+        const double keep = (double)m->nnz / ((double)m->M * (double)m->K);
+        const double Md = m->M, Nd = N;
+        r.ci_eff = 2.0 * Md * Nd * keep / (bw * Md * keep * (1.0 + 1.0 / r.pmr) + bw * Nd);
+    }
+    *out = r;
+    return US_OK;
+}

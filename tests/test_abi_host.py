@@ -1,0 +1,234 @@
+"""Host-side checks of the C-ABI library (no GPU needed).
+
+* the shared library loads and exports every symbol the headers declare;
+* us_encode is byte-identical to the oracle's encoding;
+* us_pmr agrees with the oracle's byte accounting (Eq. 1, Eq. 2);
+* every argument error is reported before any work.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import iebme
+from paper_2608_09291_amd import binding, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_symbols():
+    names = set()
+    for h in ("us.h", "us_probe.h"):
+        text = open(os.path.join(ROOT, "include", h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(us_[a-z0-9_]+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    L = binding.lib()
+    declared = _declared_symbols()
+    assert declared == set(binding.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    L = binding.lib()
+    for code in binding.STATUS:
+        assert L.us_status_string(code)
+
+
+def _assert_same_encoding(enc, ref):
+    assert enc.n_lt == ref.n_lt and enc.nnz == ref.nnz and enc.n_payload == ref.n_payload
+    assert np.array_equal(enc.bitmaps, ref.bitmaps)
+    assert np.array_equal(enc.offsets, ref.offsets)
+    assert np.array_equal(enc.payload, ref.payload)
+
+
+@pytest.mark.parametrize("M,K,s,seed,skew", [
+    (16, 64, 0.5, 0, False), (48, 192, 0.3, 1, False), (64, 256, 0.7, 2, False),
+    (32, 128, 0.0, 3, False), (32, 128, 1.0, 4, False), (80, 320, 0.9, 5, False),
+    (256, 512, 0.6, 6, True), (512, 512, 0.5, 7, False)])
+def test_encoder_matches_oracle(M, K, s, seed, skew):
+    W, _, _ = synth.random_problem(M, K, 1, s, seed, row_skew=skew)
+    _assert_same_encoding(binding.encode(W), iebme.encode(W))
+
+
+def test_encoder_matches_oracle_worked_tile(golden):
+    # A 16 x 64 tile whose union-mask rows 0..3 repeat the paper's 16-bit rows twice.
+    rows = [int(h, 16) for h in golden["union_bitmap"]["mask_rows_lsb_is_leftmost"]]
+    rng = np.random.default_rng(1)
+    W = np.zeros((16, 64), dtype=np.int8)
+    for i, h in enumerate(rows):
+        for j in range(32):
+            if (h >> (j % 16)) & 1:
+                q = int(rng.integers(4))
+                a, c = divmod(q, 2)
+                W[8 * a + i, 32 * c + j] = synth.nonzero_int4(rng, 1)[0]
+    _assert_same_encoding(binding.encode(W), iebme.encode(W))
+
+
+@pytest.mark.slow
+def test_encoder_matches_oracle_full_size():
+    w = synth.WORKLOADS["ffn_down_4096x11008_s50"]
+    W = synth.weights(w)
+    enc, ref = binding.encode(W), iebme.encode(W)
+    _assert_same_encoding(enc, ref)
+    rep = binding.pmr(enc, N=8)
+    assert rep["pmr"] == pytest.approx(iebme.pmr_report(ref, N=8)["pmr"], rel=1e-12)
+
+
+@pytest.mark.parametrize("N", [0, 1, 8, 32])
+def test_pmr_matches_oracle(N):
+    W, _, _ = synth.random_problem(128, 512, 1, 0.5, 9)
+    enc, ref = binding.encode(W), iebme.encode(W)
+    got, want = binding.pmr(enc, N), iebme.pmr_report(ref, N)
+    for key in ("nnz", "stored_values", "n_lt", "payload_stored_bytes", "bitmap_bytes",
+                "offset_bytes", "meta_bytes"):
+        assert got[key] == want[key], key
+    for key in ("payload_useful_bytes", "pmr", "pmr_stored", "ci_eff"):
+        assert got[key] == pytest.approx(want[key], rel=1e-12), key
+
+
+def test_pmr_detects_corrupt_offsets():
+    W, _, _ = synth.random_problem(32, 128, 1, 0.5, 3)
+    enc = binding.encode(W)
+    enc.offsets[2] += 4
+    r = binding.PMRReport()
+    assert binding.lib().us_pmr(ctypes.byref(enc.struct()), 0, ctypes.byref(r)) == -6
+
+
+def _encode_status(W, M=None, K=None, ldw=None, null_out=False):
+    W = np.ascontiguousarray(W, dtype=np.int8)
+    M = W.shape[0] if M is None else M
+    K = W.shape[1] if K is None else K
+    ldw = K if ldw is None else ldw
+    s = binding.IEBME()
+    out = None if null_out else ctypes.byref(s)
+    return binding.lib().us_encode(W.ctypes.data, M, K, ldw, out), s
+
+
+@pytest.mark.parametrize("case,status", [
+    ("m_not_16", -2), ("k_not_64", -2), ("zero_m", -2), ("negative_k", -2),
+    ("ldw_small", -1), ("null_out", -1), ("value_8", -3), ("value_minus_9", -3)])
+def test_encode_errors(case, status):
+    W = np.zeros((32, 128), dtype=np.int8)
+    kw = {}
+    if case == "m_not_16":
+        kw = dict(M=24)
+    elif case == "k_not_64":
+        kw = dict(K=96)
+    elif case == "zero_m":
+        kw = dict(M=0)
+    elif case == "negative_k":
+        kw = dict(K=-64)
+    elif case == "ldw_small":
+        kw = dict(ldw=64)
+    elif case == "null_out":
+        kw = dict(null_out=True)
+    elif case == "value_8":
+        W[3, 5] = 8
+    elif case == "value_minus_9":
+        W[31, 127] = -9
+    got, s = _encode_status(W, **kw)
+    assert got == status
+    assert not s.bitmaps and s.n_lt == 0          # nothing written on error
+
+
+def test_encode_null_weights():
+    s = binding.IEBME()
+    assert binding.lib().us_encode(None, 16, 64, 64, ctypes.byref(s)) == -1
+
+
+def test_encode_with_row_stride():
+    W, _, _ = synth.random_problem(32, 128, 1, 0.5, 12)
+    big = np.zeros((32, 200), dtype=np.int8)
+    big[:, :128] = W
+    big[:, 128:] = 99                 # outside the matrix: never read
+    s = binding.IEBME()
+    assert binding.lib().us_encode(big.ctypes.data, 32, 128, 200, ctypes.byref(s)) == 0
+    enc = binding.Encoded(s)
+    _assert_same_encoding(enc, iebme.encode(W))
+
+
+def _dev_struct(M=32, K=128, n_lt=None, n_payload=0, ptr=0x1000):
+    n_lt = (M // 16) * (K // 64) if n_lt is None else n_lt
+    return binding.IEBMEDev(ptr, ptr, ptr, M, K, n_lt, n_payload)
+
+
+@pytest.mark.parametrize("case,status", [
+    ("null_w", -1), ("null_x", -1), ("null_y", -1), ("scale_without_yf", -1),
+    ("m_not_16", -2), ("k_not_64", -2), ("k_too_big", -2), ("n_zero", -2), ("n_33", -2),
+    ("n_lt_wrong", -6), ("payload_odd", -6), ("payload_too_big", -6),
+    ("split_3", -1), ("variant", -1), ("misaligned_x", -1)])
+def test_spmm_argument_errors_before_launch(case, status):
+    """Every argument error returns before touching the GPU (pointers are fake)."""
+    L = binding.lib()
+    w = _dev_struct()
+    x, y, sc, yf = 0x2000, 0x3000, None, None
+    N = 8
+    opts = binding.SpmmOpts(0, 0)
+    wp = ctypes.byref(w)
+    if case == "null_w":
+        wp = None
+    elif case == "null_x":
+        x = None
+    elif case == "null_y":
+        y = None
+    elif case == "scale_without_yf":
+        sc = 0x4000
+    elif case == "m_not_16":
+        w.M = 40
+    elif case == "k_not_64":
+        w.K = 100
+    elif case == "k_too_big":
+        w.K, w.M = 131072, 16
+        w.n_lt = 2048
+    elif case == "n_zero":
+        N = 0
+    elif case == "n_33":
+        N = 33
+    elif case == "n_lt_wrong":
+        w.n_lt += 1
+    elif case == "payload_odd":
+        w.n_payload = 6
+    elif case == "payload_too_big":
+        w.n_payload = 32 * 128 + 4
+    elif case == "split_3":
+        opts.split_k = 3
+    elif case == "variant":
+        opts.variant = 1
+    elif case == "misaligned_x":
+        x = 0x2002
+    got = L.us_spmm(wp, x, N, y, sc, yf, None, 0, ctypes.byref(opts), None)
+    assert got == status
+
+
+def test_gemm_argument_errors():
+    L = binding.lib()
+    assert L.us_gemm_i8(None, 0x10, 16, 64, 1, 0x20, None) == -1
+    assert L.us_gemm_i8(0x10, 0x10, 17, 64, 1, 0x20, None) == -2
+    assert L.us_gemm_i8(0x10, 0x10, 16, 64, 33, 0x20, None) == -2
+    assert L.us_gemm_i8(0x18, 0x10, 16, 64, 1, 0x20, None) == -1
+
+
+def test_workspace_size_is_zero():
+    assert binding.workspace_size(4096, 11008, 8) == 0
+    with pytest.raises(binding.UsError):
+        binding.workspace_size(4096, 11008, 0)
+
+
+def test_probe_argument_errors():
+    L = binding.lib()
+    assert L.us_probe_read(None, 16, 0x10, None) == -1
+    assert L.us_probe_read(0x10, 15, 0x10, None) == -1
+    assert L.us_probe_copy(0x10, 0x18, 16, None) == -1
+    assert L.us_probe_spin(2 * 10 ** 9, None) == -1
+
+
+def test_pack_int4_layout():
+    Xt = np.array([[-8, 7, 0, -1]], dtype=np.int8)
+    assert binding.pack_int4(Xt).tolist() == [[0x78, 0xF0]]

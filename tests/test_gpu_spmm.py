@@ -1,0 +1,202 @@
+"""GPU parity of us_spmm (IE-BME x INT4 -> INT32, optional dequant) against the oracle.
+
+Bit-exact INT32 everywhere; the float32 dequant is one rounding on both
+sides and is compared exactly (the stated tolerance, rel 1e-6, is asserted
+too). Inputs are seeded (synth); expected values come from the oracle only.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import iebme, product
+from paper_2608_09291_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+SENTINEL = -0x5A5A5A5A
+DEQUANT_RTOL = 1e-6
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    binding.lib()          # fail loudly if the library was not built
+    return torch
+
+
+def announce(msg):
+    sys.stderr.write(f"[gpu case] {msg}\n")
+    sys.stderr.flush()
+
+
+def run_spmm(torch, W, Xt, scale=None, split_k=0, dev=None):
+    M, K = W.shape
+    N = Xt.shape[0]
+    if dev is None:
+        dev = binding.to_device(binding.encode(W))
+    xp = torch.from_numpy(binding.pack_int4(Xt)).cuda()
+    y = torch.full((N, M), SENTINEL, dtype=torch.int32, device="cuda")
+    sc = yf = None
+    if scale is not None:
+        sc = torch.from_numpy(np.asarray(scale, dtype=np.float32)).cuda()
+        yf = torch.full((N, M), float("nan"), dtype=torch.float32, device="cuda")
+    binding.spmm(dev, xp, N, y, sc, yf, split_k=split_k)
+    torch.cuda.synchronize()
+    Y = y.cpu().numpy().T
+    Yf = None if yf is None else yf.cpu().numpy().T
+    return Y, Yf
+
+
+def expect(W, Xt, scale=None):
+    Y = product.to_int32(product.matmul_c(W, Xt))
+    return Y, (None if scale is None else product.dequant(Y, scale))
+
+
+def check(Y, Yf, W, Xt, scale=None):
+    Ye, Yfe = expect(W, Xt, scale)
+    assert Y.shape == Ye.shape
+    bad = np.argwhere(Y != Ye)
+    assert bad.size == 0, f"{len(bad)} mismatches, first at {bad[0].tolist()}: {Y[tuple(bad[0])]} vs {Ye[tuple(bad[0])]}"
+    if scale is not None:
+        assert np.array_equal(Yf.view(np.uint32), Yfe.view(np.uint32))
+        np.testing.assert_allclose(Yf, Yfe, rtol=DEQUANT_RTOL, atol=0)
+
+
+SMALL = [
+    # M, K, N, sparsity, seed
+    (16, 64, 1, 0.5, 1),
+    (32, 128, 8, 0.5, 2),
+    (48, 640, 5, 0.3, 3),       # 10 LTs per row block: a batch of 8 plus a ragged 2
+    (64, 1024, 16, 0.7, 4),
+    (128, 1536, 17, 0.5, 5),    # two 16-column MFMA blocks, ragged second one
+    (96, 4096, 32, 0.6, 6),
+    (16, 8128, 3, 0.5, 7),      # 127 LTs in one row block
+    (512, 512, 8, 0.5, 8),
+    (80, 2560, 31, 0.95, 9),
+    (32, 1280, 12, 0.0, 10),    # every group active, P_t = 256
+    (32, 1280, 2, 1.0, 11),     # empty matrix: no payload at all
+]
+
+
+@pytest.mark.parametrize("M,K,N,s,seed", SMALL)
+def test_small_parity_auto(torch_cuda, M, K, N, s, seed):
+    announce(f"small auto M={M} K={K} N={N} s={s} seed={seed}")
+    W, Xt, sc = synth.random_problem(M, K, N, s, seed)
+    Y, Yf = run_spmm(torch_cuda, W, Xt, sc)
+    check(Y, Yf, W, Xt, sc)
+
+
+@pytest.mark.parametrize("split_k", [1, 2, 4, 8, 16])
+@pytest.mark.parametrize("N", [1, 8, 16, 32])
+def test_every_split(torch_cuda, split_k, N):
+    M, K = 64, 2496                                    # 39 LTs per row block
+    announce(f"split M={M} K={K} N={N} split={split_k}")
+    W, Xt, sc = synth.random_problem(M, K, N, 0.5, 100 + split_k)
+    dev = binding.to_device(binding.encode(W))
+    Y, Yf = run_spmm(torch_cuda, W, Xt, sc, split_k=split_k, dev=dev)
+    check(Y, Yf, W, Xt, sc)
+
+
+def test_row_skewed_density(torch_cuda):
+    announce("row skew M=256 K=2048 N=16")
+    W, Xt, _ = synth.random_problem(256, 2048, 16, 0.6, 21, row_skew=True)
+    Y, _ = run_spmm(torch_cuda, W, Xt)
+    check(Y, None, W, Xt)
+
+
+def test_extreme_values_at_k_max(torch_cuda):
+    """All -8 times all -8 at the largest K: |Y| = 64 K, the int32 headroom limit."""
+    K = binding.K_MAX
+    announce(f"extreme M=16 K={K} N=2")
+    W = np.full((16, K), -8, dtype=np.int8)
+    W[1::2, :] = 7
+    Xt = np.full((2, K), -8, dtype=np.int8)
+    Xt[1, ::2] = 7
+    Y, _ = run_spmm(torch_cuda, W, Xt)
+    check(Y, None, W, Xt)
+    assert Y[0, 0] == 64 * K
+
+
+def test_one_nonzero_per_tile(torch_cuda):
+    announce("one nonzero per LT M=64 K=1024 N=8")
+    rng = np.random.default_rng(5)
+    W = np.zeros((64, 1024), dtype=np.int8)
+    for mb in range(4):
+        for kb in range(16):
+            W[16 * mb + rng.integers(16), 64 * kb + rng.integers(64)] = synth.nonzero_int4(rng, 1)[0]
+    Xt = rng.integers(-8, 8, size=(8, 1024), dtype=np.int8)
+    Y, _ = run_spmm(torch_cuda, W, Xt)
+    check(Y, None, W, Xt)
+
+
+def test_alternating_signs(torch_cuda):
+    announce("alternating signs M=32 K=512 N=4")
+    i, k = np.indices((32, 512))
+    W = np.where((i + k) % 2 == 0, 7, -8).astype(np.int8)
+    W[:, 100:200] = 0
+    Xt = np.where(np.indices((4, 512)).sum(0) % 3 == 0, -8, 7).astype(np.int8)
+    Y, _ = run_spmm(torch_cuda, W, Xt)
+    check(Y, None, W, Xt)
+
+
+def test_single_position_scan(torch_cuda):
+    """Each LT row/column position alone: exercises every lane of the decode."""
+    announce("single positions M=16 K=64 N=16")
+    rng = np.random.default_rng(9)
+    Xt = rng.integers(-8, 8, size=(16, 64), dtype=np.int8)
+    for r in range(16):
+        for kk in range(0, 64, 7):
+            W = np.zeros((16, 64), dtype=np.int8)
+            W[r, kk] = -3
+            Y, _ = run_spmm(torch_cuda, W, Xt)
+            check(Y, None, W, Xt)
+
+
+def test_repeat_is_identical(torch_cuda):
+    announce("repeat M=256 K=4096 N=8")
+    W, Xt, sc = synth.random_problem(256, 4096, 8, 0.5, 33)
+    dev = binding.to_device(binding.encode(W))
+    a = run_spmm(torch_cuda, W, Xt, sc, dev=dev)
+    b = run_spmm(torch_cuda, W, Xt, sc, dev=dev)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    check(a[0], a[1], W, Xt, sc)
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads, in the launch configuration the benchmark times.
+# ---------------------------------------------------------------------------
+
+_cache = {}
+
+
+def _full(name):
+    if name not in _cache:
+        _cache.clear()
+        w = synth.WORKLOADS[name]
+        W = synth.weights(w)
+        _cache[name] = (w, W, binding.to_device(binding.encode(W)))
+    return _cache[name]
+
+
+FULL = [(name, N) for name, w in synth.WORKLOADS.items() for N in w.Ns]
+
+
+@pytest.mark.parametrize("name,N", FULL)
+def test_full_size_parity(torch_cuda, name, N):
+    announce(f"full {name} N={N}")
+    w, W, dev = _full(name)
+    Xt = synth.activations(w, N)
+    sc = synth.scales(w) if w.dequant else None
+    Y, Yf = run_spmm(torch_cuda, W, Xt, sc, dev=dev)
+    check(Y, Yf, W, Xt, sc)
+
+
+def test_longest_slice_one_wavefront(torch_cuda):
+    """127 LTs in one wavefront: the offsets span both of its offset registers."""
+    announce("one wavefront M=32 K=8128 N=3 split=1")
+    W, Xt, sc = synth.random_problem(32, 8128, 3, 0.5, 41)
+    Y, Yf = run_spmm(torch_cuda, W, Xt, sc, split_k=1)
+    check(Y, Yf, W, Xt, sc)
