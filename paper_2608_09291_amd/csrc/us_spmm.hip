@@ -79,6 +79,9 @@ __device__ __forceinline__ uint32_t dpp_row(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
 }
 
+// s_waitcnt vmcnt(0): every vector-memory load of this wavefront has returned.
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 __device__ __forceinline__ uint32_t lane_value(uint32_t v, int lane) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
@@ -208,6 +211,7 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p) {
     };
 
     const int nbatch = (nlt + kBatch - 1) / kBatch;
+    wait_vm_all();                       // the offset registers
     if (nbatch > 0) issue(0);
 
     for (int b = 0; b < nbatch; ++b) {
@@ -215,6 +219,13 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p) {
         uint32_t A0, nq;
         geometry(b, cnt, A0, nq);
         const int tb = b * kBatch;
+        uint32_t o[kBatch + 1];          // o_t of this batch's LTs (wave-uniform)
+#pragma unroll
+        for (int j = 0; j <= kBatch; ++j) o[j] = o_at(tb + min(j, cnt));
+
+        // Batch b has landed. Waiting here, before batch b+1 is issued, keeps
+        // every later use free of waits on the prefetch in flight.
+        wait_vm_all();
 
         // Commit batch b to the LDS stage.
 #pragma unroll
@@ -238,9 +249,8 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p) {
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
             if (j >= cnt) break;
-            const uint32_t ot = o_at(tb + j);
-            const uint32_t P = (o_at(tb + j + 1) - ot) >> 2;   // P_t
-            const uint32_t orel = ot - 2u * A0;                 // o_t within the stage
+            const uint32_t P = (o[j + 1] - o[j]) >> 2;          // P_t
+            const uint32_t orel = o[j] - 2u * A0;               // o_t within the stage
 
             // idx_base(i, g): popcount of rows < i plus row i's bits below 8g.
             const uint32_t mrow = st_bm[8 * j + i];
