@@ -6,7 +6,7 @@
 One step is one us_spmm call (stream the IE-BME tiles, decode, multiply,
 combine, store Y and the dequantised Y) over one copy of the encoded weight
 matrix; the encoding itself is offline, as in the paper, and is not timed.
-Every timed round queues its launches behind a bounded spin kernel, so the
+Every timed batch queues its launches behind a bounded spin kernel, so the
 GPU runs them back to back and host launch cost never enters the event
 timings; the weight copies rotate over at least 1 GiB so that none of them
 can be served from the 256 MB Infinity Cache.

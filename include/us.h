@@ -141,7 +141,7 @@ us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, const us_spmm_
  * takes the IE-BME matrix, the activations and a split-K count, and returns Y).
  *   w      : encoded matrix, device arrays
  *   x      : device, N x K row-major INT4, two values per byte along K
- *            (even k in the low nibble), 4-byte aligned
+ *            (even k in the low nibble), 16-byte aligned
  *   N      : 1..32 activation columns
  *   y      : device int32, N x M row-major (y[n * M + m] = Y[m][n])
  *   scale  : device float32[M] or NULL; with it, y_f32[n * M + m] =

@@ -8,7 +8,7 @@ fused or reordered for speed. Only ``tests/``, ``__graft_entry__.smoke()`` and
 the CPU-baseline leg of ``bench.py`` may use this package. It shares no code
 with the HIP path.
 
-Readings taken where the paper is silent (each is listed in the design doc):
+Readings taken where the paper is silent:
   * local tile (LT) 16 x 64, given only in the caption of the encoding figure;
   * R_A = C_A = 2, so Q = 4 areas of 8 x 32;
   * area index q = a * C_A + c, for row partition a and column partition c;
