@@ -34,6 +34,30 @@ DEFAULT_WORKLOAD = "ffn_down_4096x11008_s50"
 HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 1 << 30
 ROUND_LAUNCHES = 200
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_09291_amd", "csrc", "us_spmm.hip")
+
+# HBM traffic of one SpMM launch, read from rocprofv3 --pmc runs of this
+# script (one pass for FETCH_SIZE, one for WRITE_SIZE; KiB per dispatch), each
+# divided by what the same counter reads per byte for the plain copy kernel
+# (bench.py --copy-probe 268435456: FETCH_SIZE reads 0.5 KiB and WRITE_SIZE
+# 1.0 KiB per KiB copied). An entry holds only for the kernel source whose
+# SHA-256 starts with `src`; after any change to it the traffic is unknown.
+COPY_FACTOR = {"FETCH_SIZE": 0.5, "WRITE_SIZE": 1.0}
+MEASURED_TRAFFIC = {
+    ("ffn_down_4096x11008_s50", 8): dict(src="a835a49bed8c95bd", FETCH_SIZE=11409.2, WRITE_SIZE=256.0),
+}
+
+
+def measured_traffic(workload: str, N: int):
+    """Counter-derived HBM bytes per launch, or None if not measured for this kernel source."""
+    import hashlib
+    e = MEASURED_TRAFFIC.get((workload, N))
+    if e is None:
+        return None
+    with open(KERNEL_SRC, "rb") as f:
+        if not hashlib.sha256(f.read()).hexdigest().startswith(e["src"]):
+            return None
+    return int(round(sum(e[c] / COPY_FACTOR[c] for c in COPY_FACTOR) * 1024))
 
 
 def log(*a):
@@ -50,6 +74,9 @@ def parse():
     ap.add_argument("--split-k", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extras", action="store_true", help="skip the read-ceiling and dense GEMM points")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run the plain copy kernel over BYTES bytes, --steps times (the known "
+                         "byte count that calibrates the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
 
 
@@ -61,21 +88,33 @@ class Timer:
         self.stream = torch.cuda.current_stream()
 
     def run(self, launch, count: int, per_launch_host_us: float = 20.0) -> float:
-        """Total GPU milliseconds of `count` launches (launch(i) enqueues one)."""
+        """Total GPU milliseconds of `count` launches (launch(i) enqueues one).
+
+        Each batch is queued behind a spin kernel that lasts twice the
+        expected host enqueue time; a batch whose enqueue took longer than
+        the spin (the GPU may then have idled waiting for the host) is timed
+        again with a longer spin."""
         torch = self.torch
         total = 0.0
         done = 0
+        retries = 0
         while done < count:
             n = min(ROUND_LAUNCHES, count - done)
-            # Long enough for the host to queue all n launches before the GPU gets there.
-            binding.probe_spin(int(max(2e6, n * per_launch_host_us * 1e3 * 2)))
+            spin_ns = int(max(2e6, n * per_launch_host_us * 1e3 * 2))
+            binding.probe_spin(spin_ns)
             start = torch.cuda.Event(enable_timing=True)
             end = torch.cuda.Event(enable_timing=True)
+            t_host = time.perf_counter()
             start.record(self.stream)
             for i in range(n):
                 launch(done + i)
             end.record(self.stream)
+            t_host = time.perf_counter() - t_host
             end.synchronize()
+            if t_host * 1e9 > 0.9 * spin_ns and retries < 4:
+                per_launch_host_us *= 4
+                retries += 1
+                continue
             total += start.elapsed_time(end)
             done += n
         return total
@@ -184,6 +223,20 @@ def cpu_baseline(w, W, Xt, enc_bytes_alg, budget_s=12.0):
                 ms_per_call=round(med * 1e3, 3))
 
 
+def copy_probe(torch, args, timer):
+    nbytes = (args.copy_probe + 15) // 16 * 16
+    src = torch.full((nbytes,), 7, dtype=torch.uint8, device="cuda")
+    dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    ms = timer.run(lambda i: binding.probe_copy(src, dst, nbytes), args.steps)
+    torch.cuda.synchronize()
+    if not bool((dst == 7).all()):
+        raise RuntimeError("copy probe produced wrong bytes")
+    us = ms * 1e3 / args.steps
+    print(json.dumps({"probe": "copy", "bytes_read": nbytes, "bytes_written": nbytes, "steps": args.steps,
+                      "us_per_call": round(us, 3), "gbs": round(2 * nbytes / (us * 1e-6) / 1e9, 1)}),
+          flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -195,6 +248,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     binding.lib()
+    if args.copy_probe:
+        copy_probe(torch, args, Timer(torch))
+        return
     w = synth.WORKLOADS[args.workload]
     N = args.N or w.Ns[0]
     timer = Timer(torch)
@@ -250,7 +306,8 @@ def main():
         "pmr_stored": round(rep["pmr_stored"], 4),
         "ci_eff_eq2": round(rep["ci_eff"], 3),
         "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(w.name, N),
                      "kernel": "us_spmm_kernel",
                      "bytes_per_launch": r["alg_bytes"]},
         "cpu_baseline": cpu,
