@@ -13,23 +13,26 @@
 //
 //  * Staging (the paper's producer/consumer pipeline, re-cut for CDNA4). A
 //    wavefront's slice is processed in chunks of up to CH LTs, normally one.
-//    For a chunk the wavefront first reads the chunk's offsets, then requests
-//    all of its payload (16-byte buffer loads), bitmaps and activations at
-//    once: one memory round trip per chunk, with the whole machine's requests
-//    in flight together. The data is then copied into the wavefront's own LDS
-//    stage and decoded. A wavefront's LDS accesses execute in order, so no
-//    workgroup barrier is needed between staging and decoding.
+//    For a chunk the wavefront first reads the chunk's offsets, then streams
+//    its payload with 16-byte buffer loads (a few in flight, the rest issued
+//    as earlier ones land) while the bitmaps and the activation slice, which
+//    were requested together with the offsets, are copied into the
+//    wavefront's own LDS stage. A wavefront's LDS accesses execute in order,
+//    so no workgroup barrier is needed between staging and decoding.
 //
 //  * Decode (the paper's LSPD, Section VI-B). One LT (16 x 64) is decoded by
 //    one wavefront straight into the A operand of v_mfma_i32_16x16x64_i8.
 //    Lane l owns MFMA row l % 16 = 2 i + a (union-mask row i, area row a) and
-//    k-group g = l / 16, which is the G = 8 bit segment g of mask row i. The
-//    lane's idx_base (earlier rows' popcounts plus the popcount of its row
-//    before bit 8 g) comes from a DPP row scan; the same index then reads
-//    area stream q = 2a (columns 8g..8g+7) and stream q = 2a + 1 (columns
-//    32+8g..32+8g+7), which is the paper's "one rank reused across all area
+//    k-group g = l / 16, which is the G = 8 bit segment g of mask row i.
+//    idx_base is split in two: the popcount of the rows before row i (plus
+//    2 P_t for area row a = 1, whose streams start two streams later) is the
+//    same for all four segments of a row, so it is computed once per LT and
+//    chunk by a DPP scan over 16 lanes and kept in LDS as a stage bit address;
+//    each lane adds the popcount of its row below bit 8 g. The same index then
+//    reads area stream q = 2a (columns 8g..8g+7) and stream q = 2a + 1
+//    (columns 32+8g..32+8g+7), the paper's "one rank reused across all area
 //    streams". Active nibbles are placed into their byte slots with two
-//    v_perm_b32 per 8 positions, selectors taken from a 256-entry LDS table
+//    v_perm_b32 per 8 positions, selectors taken from a 256-entry table
 //    indexed by the 8-bit segment; inactive slots get selector 0x0C (zero).
 //    LTs are decoded in pairs so that two independent chains interleave.
 //
@@ -53,47 +56,105 @@
 namespace {
 
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) u32x2 lds_u2;
+typedef __attribute__((address_space(3))) u32x4 lds_u4;
 
 constexpr uint32_t kHiNib = 0xF0F0F0F0u;
 constexpr int kWindow = US_SPMM_WINDOW;                // payload loads in flight per wavefront
 constexpr int kNonTemporal = 2;                        // buffer cache policy: nt
-constexpr int kBufferDword3 = 0x00020000;           // raw buffer, 32-bit data (gfx9 family)
+constexpr int kBufferDword3 = 0x00020000;              // raw buffer, 32-bit data (gfx9 family)
+constexpr int kLutBytes = 2048;                        // 256 selector pairs, at the start of LDS
+constexpr int kMaxLds = 160 * 1024;
 
-// LDS stage of one chunk of CH LTs (per wavefront):
-//   payload : at most 512 CH bytes; the stage starts at the 16-byte boundary
-//             at or below the chunk's first byte (up to 15 bytes early) and a
-//             segment window may read 8 bytes past the last value, so at most
-//             32 CH + 2 pieces of 16 bytes are staged;
-//   bitmaps : 32 bytes per LT;
-//   X       : the chunk's activation slice, N rows of 32 bytes per LT, packed;
-//             rows are kXRowPad bytes apart so that the 16 rows read by one
-//             instruction fall in different LDS banks.
+// Selector pair for each 8-bit union-mask segment m. Slot s of the output
+// (dword 0: s = 0..3, dword 1: s = 4..7) holds segment position 2s (s < 4) or
+// 2(s-4)+1 (s >= 4). An active position of rank r takes the r-th packed
+// value: even r sits in byte r/2 of the "low" source, odd r in byte r/2 of the
+// "high" source (bytes 4..7 of v_perm_b32's 8-byte input).
+struct SelectorTable {
+    uint32_t v[512];
+};
+constexpr SelectorTable make_selectors() {
+    SelectorTable t{};
+    for (int m = 0; m < 256; ++m) {
+        uint32_t sel[2] = {0u, 0u};
+        for (int s = 0; s < 8; ++s) {
+            const int pos = s < 4 ? 2 * s : 2 * (s - 4) + 1;
+            uint32_t b = 0x0Cu;                               // v_perm: constant zero
+            if ((m >> pos) & 1) {
+                int r = 0;
+                for (int q = 0; q < pos; ++q) r += (m >> q) & 1;
+                b = (r & 1) ? 4u + (uint32_t)(r >> 1) : (uint32_t)(r >> 1);
+            }
+            sel[s >> 2] |= b << (8 * (s & 3));
+        }
+        t.v[2 * m] = sel[0];
+        t.v[2 * m + 1] = sel[1];
+    }
+    return t;
+}
+__device__ const SelectorTable kSelectors = make_selectors();
+
+// LDS stage of one chunk of CH LTs (per wavefront), in bytes from the stage start:
+//   payload : the chunk's compressed values. The stage starts at the 16-byte
+//             boundary at or below the chunk's first byte (up to 15 bytes
+//             early) and a segment window may read 8 bytes past the last
+//             value, so at most 32 CH + 2 pieces of 16 bytes are staged;
+//   bitmaps : union-mask rows, 8 dwords per LT;
+//   bases   : per LT and lane row rr = 2i + a, the LDS bit address of the
+//             first value of row i in area stream 2a (16 dwords per LT);
+//   sd      : per LT, the number of bits of one area stream (o_{t+1} - o_t);
+//   offsets : o_t of the chunk's LTs and the end offset (CH + 1 dwords);
+//   X       : the chunk's activation slice, one row of 32 bytes per LT for
+//             each activation column; rows are 16 bytes longer than the
+//             slice so that the 16 rows read by one instruction fall in
+//             different LDS banks.
 template <int CH>
 struct Chunk {
-    static constexpr int kPayBytes = 512 * CH + 64;
-    static constexpr int kPieces = kPayBytes / 16;
-    static constexpr int kLoads = (32 * CH + 2 + 63) / 64;   // 16-byte payload loads per lane
-    static constexpr int kBmWords = 8 * CH;                   // union-bitmap dwords
-    static constexpr int kBmLoads = (kBmWords + 63) / 64;
-    static constexpr int kBmOffset = kPayBytes;               // bytes into the stage
-    static constexpr int kXOffset = kPayBytes + 4 * kBmWords;
-    static_assert(kLoads * 64 >= 32 * CH + 2 && kPieces >= 32 * CH + 2, "stage size");
-    // Stage bytes for N activation columns.
-    static constexpr int kXRowWords = 8 * CH + 4;             // row stride, dwords (+16 bytes)
-    static constexpr int bytes(int N) { return kXOffset + 4 * kXRowWords * N; }
+    static constexpr int kPayPieces = 32 * CH + 2;
+    static constexpr int kLoads = (kPayPieces + 63) / 64;     // payload loads per lane
+    static constexpr int kBmOffset = 16 * kPayPieces;
+    static constexpr int kBaseOffset = kBmOffset + 32 * CH;
+    static constexpr int kSdOffset = kBaseOffset + 64 * CH;
+    static constexpr int kOffOffset = kSdOffset + 4 * CH;
+    static constexpr int kXOffset = (kOffOffset + 4 * (CH + 1) + 15) & ~15;
+    static constexpr int kXRowWords = 8 * CH + 4;
+    // Activation staging: a row of the slice is 2 CH pieces of 16 bytes; one
+    // load instruction covers kXRows rows, lane = row slot * kXSpan + piece.
+    static constexpr int kXSpan = (2 * CH <= 8) ? 8 : (2 * CH <= 16) ? 16 : (2 * CH <= 32) ? 32 : 64;
+    static constexpr int kXRows = 64 / kXSpan;
+    static constexpr int kPasses = (CH + 3) / 4;              // base passes, 4 LTs each
+    static_assert(2 * CH <= 64, "bitmap rows: one 16-byte load per half LT");
+    static_assert(2 * CH <= kXSpan, "activation row fits one row slot");
+    static constexpr int x_rows(int N) { return (N + kXRows - 1) / kXRows * kXRows; }
+    static constexpr int bytes(int N) { return kXOffset + 4 * kXRowWords * x_rows(N); }
 };
 
 struct SpmmArgs {
     const uint32_t *bm32;   // union bitmaps as dwords: LT t owns [8t, 8t + 8)
     const uint32_t *off;    // union value offsets, n_lt + 1
     const uint8_t *pay;     // compressed values
-    int32_t pay_bytes;      // buffer range: payload bytes rounded up to 16 (inside the pad)
-    const uint32_t *x32;    // activations, N rows of K/8 dwords
+    int32_t pay_bytes;      // payload bytes rounded up to 16 (inside the pad)
+    const uint8_t *x;       // activations, N rows of K/2 bytes
     int32_t *y;
     const float *scale;
     float *yf;
     int32_t M, K, N, nkb;
 };
+
+__device__ __forceinline__ uint32_t lds_load(uint32_t addr) { return *(const lds_u32 *)(size_t)addr; }
+// Two consecutive dwords at a 4-byte aligned address.
+__device__ __forceinline__ uint2 lds_load2(uint32_t addr) { return make_uint2(lds_load(addr), lds_load(addr + 4)); }
+// An 8-byte aligned pair.
+__device__ __forceinline__ uint2 lds_load_u2(uint32_t addr) {
+    const u32x2 v = *(const lds_u2 *)(size_t)addr;
+    return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ void lds_store(uint32_t addr, uint32_t v) { *(lds_u32 *)(size_t)addr = v; }
+__device__ __forceinline__ void lds_store4(uint32_t addr, u32x4 v) { *(lds_u4 *)(size_t)addr = v; }
 
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_row(uint32_t v) {
@@ -123,29 +184,10 @@ __device__ __forceinline__ uint32_t lane_value(uint32_t v, int lane) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
 
-// Selector pair for one 8-bit union-mask segment m. Slot s of the output
-// (dword 0: s = 0..3, dword 1: s = 4..7) holds segment position 2s (s < 4) or
-// 2(s-4)+1 (s >= 4). An active position of rank r takes the r-th packed
-// value: even r sits in byte r/2 of the "low" source, odd r in byte r/2 of the
-// "high" source (bytes 4..7 of v_perm_b32's 8-byte input).
-__device__ uint2 perm_selectors(uint32_t m) {
-    uint32_t sel[2] = {0u, 0u};
-    for (int s = 0; s < 8; ++s) {
-        const int pos = s < 4 ? 2 * s : 2 * (s - 4) + 1;
-        uint32_t b = 0x0Cu;                                   // v_perm: constant zero
-        if ((m >> pos) & 1u) {
-            const uint32_t r = __popc(m & ((1u << pos) - 1u));
-            b = (r & 1u) ? 4u + (r >> 1) : (r >> 1);
-        }
-        sel[s >> 2] |= b << (8 * (s & 3));
-    }
-    return make_uint2(sel[0], sel[1]);
-}
-
-// 32 bits of the staged payload starting at bit `bn` (nibble index * 4).
-__device__ __forceinline__ uint32_t stage_window(const uint32_t *st, uint32_t bn) {
-    const uint32_t d = bn >> 5;
-    return __builtin_amdgcn_alignbit(st[d + 1], st[d], bn);
+// 32 bits of LDS starting at LDS bit address bn (nibble index * 4).
+__device__ __forceinline__ uint32_t window(uint32_t bn) {
+    const uint2 d = lds_load2((bn >> 3) & ~3u);
+    return __builtin_amdgcn_alignbit(d.y, d.x, bn);
 }
 
 // Eight packed INT4 values -> the two slot dwords of one segment
@@ -157,42 +199,35 @@ __device__ __forceinline__ int2 place(uint32_t w, uint2 sel) {
                      (int32_t)__builtin_amdgcn_perm(hi, lo, sel.y));
 }
 
-// Decode one LT of the stage into the MFMA A operand of this lane.
-//   mrow   : union-mask row i of the LT (zero for a padding LT)
-//   s4orel : bit index, within the stage, of the LT's first payload value
-//   sd     : o_{t+1} - o_t = 4 P_t values; one area stream is P_t values = sd bits
-//   inj    : 2 P_t on lanes of area row a = 1, else 0 (their streams start 2 P_t later)
-__device__ __forceinline__ i32x4 decode_tile(const uint32_t *st, const uint2 *lut, uint32_t mrow,
-                                             uint32_t s4orel, uint32_t sd, uint32_t inj, int g,
-                                             uint32_t lomask) {
-    // idx_base(i, g) plus the area-row stream offset: an inclusive scan over the
-    // previous mask rows (lanes 2 i + a of a 16-lane DPP row hold rows
-    // i = 0..7; row 0 starts from inj), plus row i's bits below 8 g.
-    const uint32_t rp = __popc(mrow);
-    uint32_t ex = (uint32_t)__builtin_amdgcn_update_dpp((int)inj, (int)rp, 0x112, 0xF, 0xF, false);
-    ex += dpp_row<0x112>(ex);
-    ex += dpp_row<0x114>(ex);
-    ex += dpp_row<0x118>(ex);
-    const uint32_t idx = __popc(mrow & lomask) + ex;
-
-    const uint2 sel = lut[(mrow >> (8 * g)) & 0xFFu];
-    const uint32_t bn0 = s4orel + 4u * idx;             // stream q = 2a
-    const uint32_t bn1 = bn0 + sd;                      // stream q = 2a + 1
-    const int2 c0 = place(stage_window(st, bn0), sel);
-    const int2 c1 = place(stage_window(st, bn1), sel);
+// Decode one LT into the MFMA A operand of this lane.
+//   mrow : union-mask row i of the LT
+//   base : LDS bit address of row i's first value in area stream 2a
+//   sd   : bits of one area stream (stream 2a + 1 starts sd bits later)
+//   rot  : (8 g - 3) mod 32, so that rotating mrow right by it puts the
+//          lane's segment at bits 3..10 (the selector table's byte offset)
+__device__ __forceinline__ i32x4 decode_tile(uint32_t lut0, uint32_t mrow, uint32_t base, uint32_t sd,
+                                             uint32_t lomask, uint32_t rot) {
+    const uint32_t bn0 = base + 4u * __popc(mrow & lomask);
+    const uint32_t bn1 = bn0 + sd;
+    const uint2 sel = lds_load_u2(lut0 + (__builtin_amdgcn_alignbit(mrow, mrow, rot) & 0x7F8u));
+    const int2 c0 = place(window(bn0), sel);
+    const int2 c1 = place(window(bn1), sel);
     return (i32x4){c0.x, c0.y, c1.x, c1.y};
 }
 
-__device__ __forceinline__ i32x4 unpack_x(uint32_t x0, uint32_t x1) {
-    return (i32x4){(int32_t)((x0 << 4) & kHiNib), (int32_t)(x0 & kHiNib),
-                   (int32_t)((x1 << 4) & kHiNib), (int32_t)(x1 & kHiNib)};
+// Dwords g and g + 4 of an activation row's 8 dwords for one LT.
+__device__ __forceinline__ uint2 x_pair(uint32_t addr) { return make_uint2(lds_load(addr), lds_load(addr + 16)); }
+
+__device__ __forceinline__ i32x4 unpack_x(uint2 x) {
+    return (i32x4){(int32_t)((x.x << 4) & kHiNib), (int32_t)(x.x & kHiNib),
+                   (int32_t)((x.y << 4) & kHiNib), (int32_t)(x.y & kHiNib)};
 }
 
 template <int WPG, int NB, int CH>
 __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage_bytes) {
     using C = Chunk<CH>;
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
-    uint2 *lut = (uint2 *)lds;                               // 256 selector pairs
+    const uint32_t lds0 = (uint32_t)(size_t)(lds_u32 *)lds;  // LDS address of the dynamic block
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -205,148 +240,167 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
     const int nlt = (wave + 1) * nkb / WPG - kb0;
     const int64_t t0 = (int64_t)mb * nkb + kb0;
 
-    // Offsets of the first chunk; the selector table is built while they load.
-    uint32_t offv = p.off[t0 + min(lane, min(nlt, CH))];   // nlt = 0 reads o_{t0} only
-    for (int e = threadIdx.x; e < 256; e += 64 * WPG) lut[e] = perm_selectors((uint32_t)e);
-    __syncthreads();
-
-    // Lane roles.
+    // Lane roles in the decode.
     const int rr = lane & 15;
-    const uint32_t amask = (rr & 1) ? ~0u : 0u;            // area row partition a = 1
     const int i = rr >> 1;                                 // union-mask row
     const int g = lane >> 4;                               // segment / MFMA k-group
+    const uint32_t amask = (rr & 1) ? ~0u : 0u;            // area row partition a = 1
     const uint32_t lomask = (1u << (8 * g)) - 1u;          // mask bits before the segment
+    const uint32_t rot = (uint32_t)(8 * g + 29) & 31u;
 
-    const __amdgpu_buffer_rsrc_t rsrc =
-        __builtin_amdgcn_make_buffer_rsrc((void *)p.pay, (short)0, p.pay_bytes, kBufferDword3);
+    const uint32_t lut0 = lds0;
+    const uint32_t st = lds0 + kLutBytes + (uint32_t)(wave * stage_bytes);   // stage, LDS bytes
+    const uint32_t st_bm = st + C::kBmOffset, st_base = st + C::kBaseOffset;
+    const uint32_t st_sd = st + C::kSdOffset, st_off = st + C::kOffOffset;
+    const uint32_t st_x = st + C::kXOffset;
 
-    uint32_t *st = lds + (2048 + wave * stage_bytes) / 4;
-    uint32_t *st_bm = st + C::kBmOffset / 4;
-    uint32_t *st_x = st + C::kXOffset / 4;
-    // X stage: row n holds 8 dwords per LT; lane (n, g) reads dwords g and g + 4.
-    // Rows >= N would only feed output columns that are never stored: clamp.
-    const uint32_t *xq[NB];
+    // Activation reads in the decode: lane (column rr, k-group g) reads dwords
+    // g and g + 4 of its row's 8 dwords for the LT. Columns >= N only feed
+    // outputs that are never stored: clamp them to a staged row.
+    uint32_t xq[NB];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) xq[nb] = st_x + min(nb * 16 + rr, N - 1) * C::kXRowWords + g;
-    const int64_t xrow_bytes = p.K / 2;
-    const uint8_t *x8 = (const uint8_t *)p.x32;
+    for (int nb = 0; nb < NB; ++nb) xq[nb] = st_x + 4u * (uint32_t)(min(nb * 16 + rr, N - 1) * C::kXRowWords + g);
+
+    // Activation loads: whole rows of K/2 bytes; rows >= N read zero.
+    const int xrow_bytes = p.K / 2;
+    const __amdgpu_buffer_rsrc_t xsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void *)p.x, (short)0, N * xrow_bytes, kBufferDword3);
+    constexpr int kXLoads = (16 * NB + C::kXRows - 1) / C::kXRows;
+    const int x_slot = lane / C::kXSpan, x_piece = lane % C::kXSpan;
+    const int x_loads = (N + C::kXRows - 1) / C::kXRows;                       // wave-uniform
+    const uint32_t xv = (uint32_t)(x_slot * xrow_bytes + 16 * x_piece);
 
     i32x4 acc[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] = (i32x4){0, 0, 0, 0};
 
-    // X staging: a row of the chunk's activation slice is 2 CH pieces of 16
-    // bytes; one load instruction covers kXRowsPerLoad rows, lane = row slot *
-    // kXLaneSpan + piece (powers of two, so no division).
-    constexpr int kXLaneSpan = (2 * CH <= 8) ? 8 : (2 * CH <= 16) ? 16 : 32;
-    constexpr int kXRowsPerLoad = 64 / kXLaneSpan;
-    constexpr int kXLoads = (16 * NB + kXRowsPerLoad - 1) / kXRowsPerLoad;
-    const int x_row_slot = lane / kXLaneSpan, x_piece = lane % kXLaneSpan;
-    const int x_loads = (N + kXRowsPerLoad - 1) / kXRowsPerLoad;   // wave-uniform
-    // Requests for a chunk's bitmaps and activations; they do not depend on
-    // the offsets. Addresses are clamped into the matrix.
-    auto request_side = [&](int c0, uint32_t (&pbm)[C::kBmLoads], i32x4 (&px)[kXLoads]) {
+    // A chunk's offsets, bitmaps and activations; they are requested together
+    // (none depends on another). Addresses are clamped into the matrix.
+    uint32_t offv;
+    u32x4 pbm;
+    i32x4 px[kXLoads];
+    auto request = [&](int c0) {
         const int cnt = max(1, min(CH, nlt - c0));         // clamped: a slice may be empty
-        const int kbs = kb0 + c0;
+        offv = p.off[t0 + c0 + min(lane, cnt)];
+        pbm = *(const u32x4 *)(p.bm32 + 8 * (t0 + c0) + 4 * min(lane, 2 * cnt - 1));
+        const uint32_t xk = (uint32_t)(32 * (kb0 + c0));
 #pragma unroll
-        for (int v = 0; v < C::kBmLoads; ++v)
-            pbm[v] = p.bm32[8 * (t0 + c0) + min(lane + 64 * v, 8 * cnt - 1)];
-        const int kb = min(kbs + (min(x_piece, 2 * CH - 1) >> 1), nkb - 1);
-#pragma unroll
-        for (int u = 0; u < kXLoads; ++u) {
-            if (u < x_loads) {                             // wave-uniform
-                const int n = min(u * kXRowsPerLoad + x_row_slot, N - 1);
-                px[u] = *(const i32x4 *)(x8 + n * xrow_bytes + 32 * kb + 16 * (x_piece & 1));
-            }
-        }
+        for (int u = 0; u < kXLoads; ++u)
+            if (u < x_loads)                                // wave-uniform
+                px[u] = __builtin_amdgcn_raw_buffer_load_b128(
+                    xsrc, xv + xk + (uint32_t)(u * C::kXRows * xrow_bytes), 0, 0);
     };
 
-    uint32_t pbm[C::kBmLoads];
-    i32x4 px[kXLoads];
-    request_side(0, pbm, px);
+    // Selector table: a constant copied into LDS while the first requests fly.
+    for (int e = threadIdx.x; e < 256; e += 64 * WPG) {
+        *(lds_u2 *)(size_t)(lut0 + 8 * e) = *(const u32x2 *)&kSelectors.v[2 * e];
+    }
+    if (nlt > 0) request(0);
+    __syncthreads();
 
     auto process_chunk = [&](int c0) {
         const int cnt = min(CH, nlt - c0);
         wait_vm_all();                                     // offsets, bitmaps, activations
 
         const uint32_t ob = lane_value(offv, 0), oe = lane_value(offv, cnt);
-        const uint32_t A0 = (ob >> 1) & ~15u;              // first staged byte
+        const uint32_t A0 = (ob >> 1) & ~15u;              // first staged payload byte
         const uint32_t span = (((oe - 2u * A0) >> 3) << 2) + 8u;
-        const uint32_t nq = min((span + 15u) >> 4, (uint32_t)C::kPieces);
-        // Payload: 16-byte pieces; load u brings stage bytes [1024 u, 1024 u + 1024).
-        // At most kWindow loads are in flight per wavefront, so early pieces are
-        // not queued behind the whole machine's requests and decoding starts
-        // while the rest streams. Non-temporal: the stream does not displace
-        // the activations, which every workgroup re-reads, from L2.
+        const uint32_t nq = min((span + 15u) >> 4, (uint32_t)C::kPayPieces);
+        // Payload: 16-byte pieces from A0; load u brings stage bytes
+        // [1024 u, 1024 u + 1024). Pieces past the chunk read zero (range
+        // check) and cost no memory traffic. kWindow loads are in flight per
+        // wavefront, so early pieces are not queued behind the whole
+        // machine's requests and decoding starts while the rest streams.
+        // Non-temporal: the stream does not displace the activations, which
+        // every workgroup re-reads, from L2.
+        const __amdgpu_buffer_rsrc_t psrc = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)(p.pay + A0), (short)0, (int)min(16u * nq, (uint32_t)p.pay_bytes - A0), kBufferDword3);
         i32x4 pf[C::kLoads];
         auto load_piece = [&](int u) {
-            // The whole offset goes in the vector operand: that is the part
-            // the buffer range check sees, so a piece past the end reads 0.
-            const uint32_t piece = min((uint32_t)(lane + 64 * u), nq - 1u);
-            pf[u] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, A0 + 16u * piece, 0, kNonTemporal);
+            pf[u] = __builtin_amdgcn_raw_buffer_load_b128(psrc, (uint32_t)(16 * lane + 1024 * u), 0,
+                                                          kNonTemporal);
         };
         static_for<0, kWindow>([&](auto uc) {
             if constexpr (decltype(uc)::value < C::kLoads) load_piece(decltype(uc)::value);
         });
 
-        // Bitmaps and activations landed first (issued earlier); stage them
-        // while the payload is in flight. Bitmap words past the chunk are zero:
-        // padding LTs decode to zero and read inside the stage.
+        // Bitmaps (zero past the chunk), offsets and activations into the stage.
+        if (lane < 2 * CH) lds_store4(st_bm + 16 * lane, lane < 2 * cnt ? pbm : (u32x4){0u, 0u, 0u, 0u});
+        if (lane <= CH) lds_store(st_off + 4 * lane, offv);
+        if (x_piece < 2 * CH) {
 #pragma unroll
-        for (int v = 0; v < C::kBmLoads; ++v)
-            if (lane + 64 * v < C::kBmWords) st_bm[lane + 64 * v] = lane + 64 * v < 8 * cnt ? pbm[v] : 0u;
-#pragma unroll
-        for (int u = 0; u < kXLoads; ++u) {
-            const int n = u * kXRowsPerLoad + x_row_slot;
-            if (u < x_loads && n < N && x_piece < 2 * CH) *(i32x4 *)(st_x + n * C::kXRowWords + 4 * x_piece) = px[u];
+            for (int u = 0; u < kXLoads; ++u)
+                if (u < x_loads)
+                    lds_store4(st_x + 4u * (uint32_t)((u * C::kXRows + x_slot) * C::kXRowWords) + 16 * x_piece,
+                               (u32x4)px[u]);
         }
 
-        // Bit address, within the stage, of payload value 0 of the whole matrix.
-        const uint32_t s4base = 4u * (0u - 2u * A0);
-        auto o_at = [&](int j) { return lane_value(offv, j); };
-        auto decode_one = [&](int j) {
-            const uint32_t oj = o_at(j), sd = o_at(j + 1) - oj;
-            const i32x4 A = decode_tile(st, lut, st_bm[8 * j + i], s4base + 4u * oj, sd, amask & (sd >> 1),
-                                        g, lomask);
+        // Row bases: lanes 16 jj + rr handle LT j = 4 pass + jj, mask row i,
+        // area row a. The scan over the 16 lanes of a DPP row starts area row
+        // a = 1 at 2 P_t (its streams follow streams 0 and 1) and adds the
+        // popcounts of the rows before i.
+        // LDS bit address of payload value v of the matrix: sbase + 4 v.
+        const uint32_t sbase = 8u * st - 8u * A0;
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                const uint32_t *xl = xq[nb] + 8 * j;
-                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, unpack_x(xl[0], xl[4]), acc[nb], 0, 0, 0);
+        for (int ps = 0; ps < C::kPasses; ++ps) {
+            const int j = 4 * ps + (lane >> 4);
+            const int jc = min(j, CH - 1);
+            const uint32_t mrow = lds_load(st_bm + 4 * (8 * jc + i));
+            const uint2 o = lds_load2(st_off + 4 * jc);
+            const uint32_t rp = __popc(mrow);
+            const uint32_t inj = amask & ((o.y - o.x) >> 1);
+            uint32_t ex = (uint32_t)__builtin_amdgcn_update_dpp((int)inj, (int)rp, 0x112, 0xF, 0xF, false);
+            ex += dpp_row<0x112>(ex);
+            ex += dpp_row<0x114>(ex);
+            ex += dpp_row<0x118>(ex);
+            if (j < CH) {
+                lds_store(st_base + 4 * (16 * j + rr), sbase + 4u * (o.x + ex));
+                if (rr == 0) lds_store(st_sd + 4 * j, o.y - o.x);
             }
+        }
+        // LT k can be decoded once the pieces holding its windows have landed:
+        // o_{k+1} - 2 A0 + 16 <= 2048 (u + 1), i.e. after load u = need_k.
+        const uint32_t need = (lds_load(st_off + 4 * min(lane + 1, CH)) - 2u * A0 + 15u) >> 11;
+
+        auto decode_one = [&](int j) {
+            const uint32_t mrow = lds_load(st_bm + 4 * (8 * j + i));
+            const uint32_t base = lds_load(st_base + 4 * (16 * j + rr));
+            const uint32_t sd = lds_load(st_sd + 4 * j);
+            const i32x4 A = decode_tile(lut0, mrow, base, sd, lomask, rot);
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, unpack_x(x_pair(xq[nb] + 32 * j)), acc[nb],
+                                                               0, 0, 0);
         };
         auto decode_two = [&](int j) {
-            const uint32_t o0 = o_at(j), o1 = o_at(j + 1), o2 = o_at(j + 2);
-            const uint32_t sd0 = o1 - o0, sd1 = o2 - o1;
-            const i32x4 A0v = decode_tile(st, lut, st_bm[8 * j + i], s4base + 4u * o0, sd0,
-                                          amask & (sd0 >> 1), g, lomask);
-            const i32x4 A1v = decode_tile(st, lut, st_bm[8 * (j + 1) + i], s4base + 4u * o1, sd1,
-                                          amask & (sd1 >> 1), g, lomask);
+            const uint32_t m0 = lds_load(st_bm + 4 * (8 * j + i));
+            const uint32_t m1 = lds_load(st_bm + 4 * (8 * j + 8 + i));
+            const uint32_t b0 = lds_load(st_base + 4 * (16 * j + rr));
+            const uint32_t b1 = lds_load(st_base + 4 * (16 * j + 16 + rr));
+            const uint2 sd = lds_load2(st_sd + 4 * j);
+            const i32x4 A0v = decode_tile(lut0, m0, b0, sd.x, lomask, rot);
+            const i32x4 A1v = decode_tile(lut0, m1, b1, sd.y, lomask, rot);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
-                const uint32_t *xl = xq[nb] + 8 * j;
-                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0v, unpack_x(xl[0], xl[4]), acc[nb], 0, 0, 0);
-                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1v, unpack_x(xl[8], xl[12]), acc[nb], 0, 0, 0);
+                const uint32_t xl = xq[nb] + 32 * j;
+                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0v, unpack_x(x_pair(xl)), acc[nb], 0, 0, 0);
+                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1v, unpack_x(x_pair(xl + 32)), acc[nb], 0, 0, 0);
             }
         };
 
         // The payload lands in issue order: after load u, stage bytes
-        // [0, 1024 (u + 1)) are present, so every LT whose windows end there
-        // (o_{t+1} - 2 A0 + 16 <= 2048 (u + 1) values) can be decoded.
+        // [0, 1024 (u + 1)) are present, so LTs with need <= u can be decoded.
         int j = 0;
         static_for<0, C::kLoads>([&](auto uc) {
             constexpr int u = decltype(uc)::value;
             constexpr int later = (kWindow - 1 < C::kLoads - 1 - u) ? kWindow - 1 : C::kLoads - 1 - u;
             wait_vm<later>();                              // piece u has landed
             if constexpr (u + kWindow < C::kLoads) load_piece(u + kWindow);
-            const uint32_t piece = (uint32_t)(lane + 64 * u);
-            if (piece < nq) *(i32x4 *)(st + 4 * piece) = pf[u];
+            if (u + 1 < C::kLoads || lane + 64 * u < C::kPayPieces) lds_store4(st + 1024 * u + 16 * lane, (u32x4)pf[u]);
             __asm__ volatile("" ::: "memory");
             if constexpr (u + 1 < C::kLoads) {
-                const uint32_t lim = 2u * A0 + 2048u * (u + 1) - 16u;   // wraps only when ready is unprovable
-                while (j + 1 < cnt && o_at(j + 2) <= lim) {
-                    decode_two(j);
-                    j += 2;
-                }
+                const int ready = __builtin_popcountll(__builtin_amdgcn_ballot_w64(lane < cnt && need <= (uint32_t)u));
+                for (; j + 1 < ready; j += 2) decode_two(j);
             } else {
                 for (; j + 1 < cnt; j += 2) decode_two(j);
                 if (j < cnt) decode_one(j);
@@ -354,12 +408,8 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
         });
         __asm__ volatile("" ::: "memory");
 
-        // Next chunk (long slices only): offsets, then its side data.
-        const int nnext = nlt - c0 - CH;
-        if (nnext > 0) {
-            offv = p.off[t0 + c0 + CH + min(lane, min(nnext, CH))];
-            request_side(c0 + CH, pbm, px);
-        }
+        // Next chunk (long slices only).
+        if (nlt - c0 - CH > 0) request(c0 + CH);
     };
     // The first chunk is straight-line code after the prologue, so every
     // wait above counts loads exactly; later chunks only occur for long slices.
@@ -367,41 +417,34 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
     for (int c0 = CH; c0 < nlt; c0 += CH) process_chunk(c0);
 
     // Split-K combine: each wavefront leaves its 16 x (16 NB) partial in its
-    // own stage; after the barrier all threads sum the WPG partials.
-    // MFMA result layout: lane l, element v is row 4 (l / 16) + v, column l % 16.
-    int32_t *red = (int32_t *)st;
+    // own stage, in MFMA result layout (lane l, element v: row 4 (l / 16) + v,
+    // column l % 16); after the barrier the first 16 N threads sum the WPG
+    // partials of one output each.
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int rho = 4 * g + v;
-            const int r = 8 * (rho & 1) + (rho >> 1);         // MFMA row 2i + a -> W row 8a + i
-            red[r * (16 * NB) + nb * 16 + rr] = acc[nb][v];
-        }
+    for (int nb = 0; nb < NB; ++nb) lds_store4(st + 16 * (64 * nb + lane), (u32x4)acc[nb]);
     __syncthreads();
 
-    const int64_t M = p.M;
     for (int e = threadIdx.x; e < 16 * N; e += 64 * WPG) {
         const int r = e & 15, n = e >> 4;
+        const int R = 2 * (r & 7) + (r >> 3);                 // W row 8a + i is MFMA row 2i + a
+        const uint32_t idx = 4u * (uint32_t)(4 * (64 * (n >> 4) + 16 * (R >> 2) + (n & 15)) + (R & 3));
         int32_t s = 0;
 #pragma unroll
-        for (int w = 0; w < WPG; ++w) s += ((const int32_t *)(lds + (2048 + w * stage_bytes) / 4))[r * (16 * NB) + n];
+        for (int w = 0; w < WPG; ++w) s += (int32_t)lds_load(lds0 + kLutBytes + (uint32_t)(w * stage_bytes) + idx);
         const int32_t yv = s >> 8;                            // exact: s = 256 Y
         const int64_t m = (int64_t)mb * 16 + r;
+        const int64_t M = p.M;
         p.y[n * M + m] = yv;
         if (p.scale) p.yf[n * M + m] = (float)yv * p.scale[m];
     }
 }
-
-constexpr int kLutBytes = 2048;
-constexpr int kMaxLds = 160 * 1024;
 
 template <int CH>
 int stage_bytes(int N) { return (Chunk<CH>::bytes(N) + 15) & ~15; }
 
 int lds_bytes(int ch, int N, int wpg) {
     const int st = ch == 16 ? stage_bytes<16>(N)
-                 : ch == 12 ? stage_bytes<12>(N)
+                 : ch == 11 ? stage_bytes<11>(N)
                  : ch == 8  ? stage_bytes<8>(N)
                             : stage_bytes<4>(N);
     return kLutBytes + wpg * st;
@@ -434,7 +477,7 @@ hipError_t launch_cfg(int wpg, int ch, const SpmmArgs &a, hipStream_t s) {
     if (a.N > 16) return ch == 8 ? launch_spmm_wpg<2, 8>(wpg, a, s) : launch_spmm_wpg<2, 4>(wpg, a, s);
     switch (ch) {
         case 16: return launch_spmm_wpg<1, 16>(wpg, a, s);
-        case 12: return launch_spmm_wpg<1, 12>(wpg, a, s);
+        case 11: return launch_spmm_wpg<1, 11>(wpg, a, s);
         case 8: return launch_spmm_wpg<1, 8>(wpg, a, s);
         default: return launch_spmm_wpg<1, 4>(wpg, a, s);
     }
@@ -442,12 +485,12 @@ hipError_t launch_cfg(int wpg, int ch, const SpmmArgs &a, hipStream_t s) {
 
 bool aligned(const void *ptr, uintptr_t n) { return ((uintptr_t)ptr % n) == 0; }
 
-// Chunk length for wpg slices: the smallest of 4, 8, 12, 16 LTs (4 or 8 with
+// Chunk length for wpg slices: the smallest of 4, 8, 11, 16 LTs (4 or 8 with
 // two MFMA column blocks) that holds a whole slice and fits LDS; else the
 // largest that fits (the slice then takes several chunks). 4 always fits.
 int pick_chunk(int nkb, int N, int wpg) {
     const int slice = (nkb + wpg - 1) / wpg;
-    const int cands[4] = {4, 8, 12, 16};
+    const int cands[4] = {4, 8, 11, 16};
     const int nc = N > 16 ? 2 : 4;
     int best = 0;
     for (int c = 0; c < nc; ++c) {
@@ -530,7 +573,7 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     // outside it (then it reads zeros). Rounding up stays within the
     // US_PAYLOAD_PAD bytes that follow the payload.
     a.pay_bytes = (int32_t)((((w->n_payload + 1) / 2) + 15) & ~(int64_t)15);
-    a.x32 = (const uint32_t *)x;
+    a.x = x;
     a.y = y;
     a.scale = scale;
     a.yf = y_f32;
