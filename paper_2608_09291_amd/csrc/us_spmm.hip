@@ -66,7 +66,7 @@ constexpr uint32_t kHiNib = 0xF0F0F0F0u;
 constexpr int kWindow = US_SPMM_WINDOW;                // payload loads in flight per wavefront
 constexpr int kNonTemporal = 2;                        // buffer cache policy: nt
 constexpr int kBufferDword3 = 0x00020000;              // raw buffer, 32-bit data (gfx9 family)
-constexpr int kLutBytes = 2048;                        // 256 selector pairs, at the start of LDS
+constexpr int kLutBytes = 2048;                        // 256 selector pairs (static LDS)
 constexpr int kMaxLds = 160 * 1024;
 
 // Selector pair for each 8-bit union-mask segment m. Slot s of the output
@@ -104,6 +104,8 @@ __device__ const SelectorTable kSelectors = make_selectors();
 //             early) and a segment window may read 8 bytes past the last
 //             value, so at most 32 CH + 2 pieces of 16 bytes are staged;
 //   bitmaps : union-mask rows, 8 dwords per LT;
+//             (this and the next three arrays have room for a whole number
+//             of 4-LT passes; entries past the chunk are never decoded)
 //   bases   : per LT and lane row rr = 2i + a, the LDS bit address of the
 //             first value of row i in area stream 2a (16 dwords per LT);
 //   sd      : per LT, the number of bits of one area stream (o_{t+1} - o_t);
@@ -116,17 +118,18 @@ template <int CH>
 struct Chunk {
     static constexpr int kPayPieces = 32 * CH + 2;
     static constexpr int kLoads = (kPayPieces + 63) / 64;     // payload loads per lane
+    static constexpr int kPasses = (CH + 3) / 4;              // base passes, 4 LTs each
+    static constexpr int kLtPad = 4 * kPasses;                // per-LT arrays padded to whole passes
     static constexpr int kBmOffset = 16 * kPayPieces;
-    static constexpr int kBaseOffset = kBmOffset + 32 * CH;
-    static constexpr int kSdOffset = kBaseOffset + 64 * CH;
-    static constexpr int kOffOffset = kSdOffset + 4 * CH;
-    static constexpr int kXOffset = (kOffOffset + 4 * (CH + 1) + 15) & ~15;
+    static constexpr int kBaseOffset = kBmOffset + 32 * kLtPad;
+    static constexpr int kSdOffset = kBaseOffset + 64 * kLtPad;
+    static constexpr int kOffOffset = kSdOffset + 4 * kLtPad;
+    static constexpr int kXOffset = (kOffOffset + 4 * (kLtPad + 1) + 15) & ~15;
     static constexpr int kXRowWords = 8 * CH + 4;
     // Activation staging: a row of the slice is 2 CH pieces of 16 bytes; one
     // load instruction covers kXRows rows, lane = row slot * kXSpan + piece.
     static constexpr int kXSpan = (2 * CH <= 8) ? 8 : (2 * CH <= 16) ? 16 : (2 * CH <= 32) ? 32 : 64;
     static constexpr int kXRows = 64 / kXSpan;
-    static constexpr int kPasses = (CH + 3) / 4;              // base passes, 4 LTs each
     static_assert(2 * CH <= 64, "bitmap rows: one 16-byte load per half LT");
     static_assert(2 * CH <= kXSpan, "activation row fits one row slot");
     static constexpr int x_rows(int N) { return (N + kXRows - 1) / kXRows * kXRows; }
@@ -205,11 +208,12 @@ __device__ __forceinline__ int2 place(uint32_t w, uint2 sel) {
 //   sd   : bits of one area stream (stream 2a + 1 starts sd bits later)
 //   rot  : (8 g - 3) mod 32, so that rotating mrow right by it puts the
 //          lane's segment at bits 3..10 (the selector table's byte offset)
-__device__ __forceinline__ i32x4 decode_tile(uint32_t lut0, uint32_t mrow, uint32_t base, uint32_t sd,
+__device__ __forceinline__ i32x4 decode_tile(const u32x2 *lut, uint32_t mrow, uint32_t base, uint32_t sd,
                                              uint32_t lomask, uint32_t rot) {
     const uint32_t bn0 = base + 4u * __popc(mrow & lomask);
     const uint32_t bn1 = bn0 + sd;
-    const uint2 sel = lds_load_u2(lut0 + (__builtin_amdgcn_alignbit(mrow, mrow, rot) & 0x7F8u));
+    const u32x2 sv = *(const u32x2 *)((const char *)lut + (__builtin_amdgcn_alignbit(mrow, mrow, rot) & 0x7F8u));
+    const uint2 sel = make_uint2(sv.x, sv.y);
     const int2 c0 = place(window(bn0), sel);
     const int2 c1 = place(window(bn1), sel);
     return (i32x4){c0.x, c0.y, c1.x, c1.y};
@@ -227,6 +231,7 @@ template <int WPG, int NB, int CH>
 __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage_bytes) {
     using C = Chunk<CH>;
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
+    __shared__ u32x2 lut[256];                               // selector table
     const uint32_t lds0 = (uint32_t)(size_t)(lds_u32 *)lds;  // LDS address of the dynamic block
 
     const int lane = threadIdx.x & 63;
@@ -248,8 +253,7 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
     const uint32_t lomask = (1u << (8 * g)) - 1u;          // mask bits before the segment
     const uint32_t rot = (uint32_t)(8 * g + 29) & 31u;
 
-    const uint32_t lut0 = lds0;
-    const uint32_t st = lds0 + kLutBytes + (uint32_t)(wave * stage_bytes);   // stage, LDS bytes
+    const uint32_t st = lds0 + (uint32_t)(wave * stage_bytes);   // stage, LDS bytes
     const uint32_t st_bm = st + C::kBmOffset, st_base = st + C::kBaseOffset;
     const uint32_t st_sd = st + C::kSdOffset, st_off = st + C::kOffOffset;
     const uint32_t st_x = st + C::kXOffset;
@@ -293,7 +297,7 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
 
     // Selector table: a constant copied into LDS while the first requests fly.
     for (int e = threadIdx.x; e < 256; e += 64 * WPG) {
-        *(lds_u2 *)(size_t)(lut0 + 8 * e) = *(const u32x2 *)&kSelectors.v[2 * e];
+        lut[e] = *(const u32x2 *)&kSelectors.v[2 * e];
     }
     if (nlt > 0) request(0);
     __syncthreads();
@@ -344,48 +348,54 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
 #pragma unroll
         for (int ps = 0; ps < C::kPasses; ++ps) {
             const int j = 4 * ps + (lane >> 4);
-            const int jc = min(j, CH - 1);
-            const uint32_t mrow = lds_load(st_bm + 4 * (8 * jc + i));
-            const uint2 o = lds_load2(st_off + 4 * jc);
+            const uint32_t mrow = lds_load(st_bm + 4 * (8 * j + i));
+            const uint2 o = lds_load2(st_off + 4 * j);
             const uint32_t rp = __popc(mrow);
             const uint32_t inj = amask & ((o.y - o.x) >> 1);
             uint32_t ex = (uint32_t)__builtin_amdgcn_update_dpp((int)inj, (int)rp, 0x112, 0xF, 0xF, false);
             ex += dpp_row<0x112>(ex);
             ex += dpp_row<0x114>(ex);
             ex += dpp_row<0x118>(ex);
-            if (j < CH) {
-                lds_store(st_base + 4 * (16 * j + rr), sbase + 4u * (o.x + ex));
-                if (rr == 0) lds_store(st_sd + 4 * j, o.y - o.x);
-            }
+            lds_store(st_base + 4 * (16 * j + rr), sbase + 4u * (o.x + ex));
+            if (rr == 0) lds_store(st_sd + 4 * j, o.y - o.x);
         }
         // LT k can be decoded once the pieces holding its windows have landed:
         // o_{k+1} - 2 A0 + 16 <= 2048 (u + 1), i.e. after load u = need_k.
         const uint32_t need = (lds_load(st_off + 4 * min(lane + 1, CH)) - 2u * A0 + 15u) >> 11;
 
-        auto decode_one = [&](int j) {
-            const uint32_t mrow = lds_load(st_bm + 4 * (8 * j + i));
-            const uint32_t base = lds_load(st_base + 4 * (16 * j + rr));
-            const uint32_t sd = lds_load(st_sd + 4 * j);
-            const i32x4 A = decode_tile(lut0, mrow, base, sd, lomask, rot);
+        // LDS addresses of the next LT's mask row, row base, stream length and
+        // activations for this lane; they advance as LTs are decoded. The
+        // stream-length address is the same on every lane; it is kept in a
+        // vector register so that the loop needs no scalar-to-vector moves.
+        uint32_t a_bm = st_bm + 4 * i, a_base = st_base + 4 * rr, a_sd;
+        __asm__("v_mov_b32 %0, %1" : "=v"(a_sd) : "s"(st_sd));
+        uint32_t a_x[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) a_x[nb] = xq[nb];
+        auto decode_one = [&]() {
+            const uint32_t mrow = lds_load(a_bm);
+            const uint32_t base = lds_load(a_base);
+            const uint32_t sd = lds_load(a_sd);
+            const i32x4 A = decode_tile(lut, mrow, base, sd, lomask, rot);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
-                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, unpack_x(x_pair(xq[nb] + 32 * j)), acc[nb],
-                                                               0, 0, 0);
+                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, unpack_x(x_pair(a_x[nb])), acc[nb], 0, 0, 0);
         };
-        auto decode_two = [&](int j) {
-            const uint32_t m0 = lds_load(st_bm + 4 * (8 * j + i));
-            const uint32_t m1 = lds_load(st_bm + 4 * (8 * j + 8 + i));
-            const uint32_t b0 = lds_load(st_base + 4 * (16 * j + rr));
-            const uint32_t b1 = lds_load(st_base + 4 * (16 * j + 16 + rr));
-            const uint2 sd = lds_load2(st_sd + 4 * j);
-            const i32x4 A0v = decode_tile(lut0, m0, b0, sd.x, lomask, rot);
-            const i32x4 A1v = decode_tile(lut0, m1, b1, sd.y, lomask, rot);
+        auto decode_two = [&]() {
+            const uint32_t m0 = lds_load(a_bm), m1 = lds_load(a_bm + 32);
+            const uint32_t b0 = lds_load(a_base), b1 = lds_load(a_base + 64);
+            const uint2 sd = lds_load2(a_sd);
+            const i32x4 A0v = decode_tile(lut, m0, b0, sd.x, lomask, rot);
+            const i32x4 A1v = decode_tile(lut, m1, b1, sd.y, lomask, rot);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
-                const uint32_t xl = xq[nb] + 32 * j;
-                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0v, unpack_x(x_pair(xl)), acc[nb], 0, 0, 0);
-                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1v, unpack_x(x_pair(xl + 32)), acc[nb], 0, 0, 0);
+                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0v, unpack_x(x_pair(a_x[nb])), acc[nb], 0, 0, 0);
+                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1v, unpack_x(x_pair(a_x[nb] + 32)), acc[nb], 0, 0, 0);
+                a_x[nb] += 64;
             }
+            a_bm += 64;
+            a_base += 128;
+            a_sd += 8;
         };
 
         // The payload lands in issue order: after load u, stage bytes
@@ -400,10 +410,10 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
             __asm__ volatile("" ::: "memory");
             if constexpr (u + 1 < C::kLoads) {
                 const int ready = __builtin_popcountll(__builtin_amdgcn_ballot_w64(lane < cnt && need <= (uint32_t)u));
-                for (; j + 1 < ready; j += 2) decode_two(j);
+                for (; j + 1 < ready; j += 2) decode_two();
             } else {
-                for (; j + 1 < cnt; j += 2) decode_two(j);
-                if (j < cnt) decode_one(j);
+                for (; j + 1 < cnt; j += 2) decode_two();
+                if (j < cnt) decode_one();
             }
         });
         __asm__ volatile("" ::: "memory");
@@ -430,7 +440,7 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
         const uint32_t idx = 4u * (uint32_t)(4 * (64 * (n >> 4) + 16 * (R >> 2) + (n & 15)) + (R & 3));
         int32_t s = 0;
 #pragma unroll
-        for (int w = 0; w < WPG; ++w) s += (int32_t)lds_load(lds0 + kLutBytes + (uint32_t)(w * stage_bytes) + idx);
+        for (int w = 0; w < WPG; ++w) s += (int32_t)lds_load(lds0 + (uint32_t)(w * stage_bytes) + idx);
         const int32_t yv = s >> 8;                            // exact: s = 256 Y
         const int64_t m = (int64_t)mb * 16 + r;
         const int64_t M = p.M;
@@ -455,10 +465,10 @@ hipError_t launch_spmm(const SpmmArgs &a, hipStream_t s) {
     auto kern = us_spmm_kernel<WPG, NB, CH>;
     // Allow more than 64 KB of dynamic LDS (set once per instantiation).
     static const hipError_t attr =
-        hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds);
+        hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes);
     (void)attr;
     const int st = stage_bytes<CH>(a.N);
-    hipLaunchKernelGGL(kern, dim3(a.M / 16), dim3(64 * WPG), kLutBytes + WPG * st, s, a, st);
+    hipLaunchKernelGGL(kern, dim3(a.M / 16), dim3(64 * WPG), WPG * st, s, a, st);
     return hipGetLastError();
 }
 
