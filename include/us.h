@@ -124,7 +124,8 @@ typedef struct {
 
 typedef struct {
     int32_t split_k;  /* K slices per 16-row block, one wavefront each:
-                         0 = automatic, else 1, 2, 4, 8 or 16            */
+                         0 = automatic, else 1, 2, 4, 8 or 16; halved
+                         while it exceeds K / 64 (one LT per slice)      */
     int32_t variant;  /* reserved, must be 0                             */
 } us_spmm_opts;
 

@@ -69,34 +69,25 @@ constexpr int kBufferDword3 = 0x00020000;              // raw buffer, 32-bit dat
 constexpr int kLutBytes = 2048;                        // 256 selector pairs (static LDS)
 constexpr int kMaxLds = 160 * 1024;
 
-// Selector pair for each 8-bit union-mask segment m. Slot s of the output
+// Selector pair for one 8-bit union-mask segment m. Slot s of the output
 // (dword 0: s = 0..3, dword 1: s = 4..7) holds segment position 2s (s < 4) or
 // 2(s-4)+1 (s >= 4). An active position of rank r takes the r-th packed
 // value: even r sits in byte r/2 of the "low" source, odd r in byte r/2 of the
 // "high" source (bytes 4..7 of v_perm_b32's 8-byte input).
-struct SelectorTable {
-    uint32_t v[512];
-};
-constexpr SelectorTable make_selectors() {
-    SelectorTable t{};
-    for (int m = 0; m < 256; ++m) {
-        uint32_t sel[2] = {0u, 0u};
-        for (int s = 0; s < 8; ++s) {
-            const int pos = s < 4 ? 2 * s : 2 * (s - 4) + 1;
-            uint32_t b = 0x0Cu;                               // v_perm: constant zero
-            if ((m >> pos) & 1) {
-                int r = 0;
-                for (int q = 0; q < pos; ++q) r += (m >> q) & 1;
-                b = (r & 1) ? 4u + (uint32_t)(r >> 1) : (uint32_t)(r >> 1);
-            }
-            sel[s >> 2] |= b << (8 * (s & 3));
+__device__ u32x2 perm_selectors(uint32_t m) {
+    uint32_t sel[2] = {0u, 0u};
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        const int pos = s < 4 ? 2 * s : 2 * (s - 4) + 1;
+        uint32_t b = 0x0Cu;                                   // v_perm: constant zero
+        if ((m >> pos) & 1u) {
+            const uint32_t r = __popc(m & ((1u << pos) - 1u));
+            b = (r & 1u) ? 4u + (r >> 1) : (r >> 1);
         }
-        t.v[2 * m] = sel[0];
-        t.v[2 * m + 1] = sel[1];
+        sel[s >> 2] |= b << (8 * (s & 3));
     }
-    return t;
+    return (u32x2){sel[0], sel[1]};
 }
-__device__ const SelectorTable kSelectors = make_selectors();
 
 // LDS stage of one chunk of CH LTs (per wavefront), in bytes from the stage start:
 //   payload : the chunk's compressed values. The stage starts at the 16-byte
@@ -126,14 +117,9 @@ struct Chunk {
     static constexpr int kOffOffset = kSdOffset + 4 * kLtPad;
     static constexpr int kXOffset = (kOffOffset + 4 * (kLtPad + 1) + 15) & ~15;
     static constexpr int kXRowWords = 8 * CH + 4;
-    // Activation staging: a row of the slice is 2 CH pieces of 16 bytes; one
-    // load instruction covers kXRows rows, lane = row slot * kXSpan + piece.
-    static constexpr int kXSpan = (2 * CH <= 8) ? 8 : (2 * CH <= 16) ? 16 : (2 * CH <= 32) ? 32 : 64;
-    static constexpr int kXRows = 64 / kXSpan;
+    static constexpr int kXPieces = 2 * CH;                   // 16-byte pieces of one activation row
     static_assert(2 * CH <= 64, "bitmap rows: one 16-byte load per half LT");
-    static_assert(2 * CH <= kXSpan, "activation row fits one row slot");
-    static constexpr int x_rows(int N) { return (N + kXRows - 1) / kXRows * kXRows; }
-    static constexpr int bytes(int N) { return kXOffset + 4 * kXRowWords * x_rows(N); }
+    static constexpr int bytes(int N) { return kXOffset + 4 * kXRowWords * N; }
 };
 
 struct SpmmArgs {
@@ -239,7 +225,8 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
     const int mb = blockIdx.x;
     const int N = p.N;
 
-    // This wavefront's K slice: LTs t0 .. t0 + nlt - 1 of row block mb.
+    // This wavefront's K slice: LTs t0 .. t0 + nlt - 1 of row block mb
+    // (nlt >= 1 because WPG <= K / 64).
     const int nkb = p.nkb;
     const int kb0 = wave * nkb / WPG;
     const int nlt = (wave + 1) * nkb / WPG - kb0;
@@ -269,10 +256,19 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
     const int xrow_bytes = p.K / 2;
     const __amdgpu_buffer_rsrc_t xsrc =
         __builtin_amdgcn_make_buffer_rsrc((void *)p.x, (short)0, N * xrow_bytes, kBufferDword3);
-    constexpr int kXLoads = (16 * NB + C::kXRows - 1) / C::kXRows;
-    const int x_slot = lane / C::kXSpan, x_piece = lane % C::kXSpan;
-    const int x_loads = (N + C::kXRows - 1) / C::kXRows;                       // wave-uniform
-    const uint32_t xv = (uint32_t)(x_slot * xrow_bytes + 16 * x_piece);
+    // Activation staging: the chunk's N x 2 CH pieces of 16 bytes, piece
+    // q = lane + 64 u is row q / (2 CH), piece q % (2 CH). Only the loads
+    // that carry pieces are issued: the texture path, not HBM, limits how
+    // fast a CU takes them in at the start of the kernel.
+    constexpr int kXLoads = (16 * NB * C::kXPieces + 63) / 64;
+    const int x_loads = (N * C::kXPieces + 63) / 64;                           // wave-uniform
+    uint32_t xv[kXLoads], xs[kXLoads];                     // global byte offset, LDS address
+#pragma unroll
+    for (int u = 0; u < kXLoads; ++u) {
+        const int q = lane + 64 * u, n = q / C::kXPieces, pj = q % C::kXPieces;
+        xv[u] = (uint32_t)(n * xrow_bytes + 16 * pj);      // rows >= N fall outside the range: zero
+        xs[u] = n < N ? st_x + 4u * (uint32_t)(n * C::kXRowWords) + 16u * (uint32_t)pj : 0u;
+    }
 
     i32x4 acc[NB];
 #pragma unroll
@@ -290,24 +286,30 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
         const uint32_t xk = (uint32_t)(32 * (kb0 + c0));
 #pragma unroll
         for (int u = 0; u < kXLoads; ++u)
-            if (u < x_loads)                                // wave-uniform
-                px[u] = __builtin_amdgcn_raw_buffer_load_b128(
-                    xsrc, xv + xk + (uint32_t)(u * C::kXRows * xrow_bytes), 0, 0);
+            if (u < x_loads) px[u] = __builtin_amdgcn_raw_buffer_load_b128(xsrc, xv[u] + xk, 0, 0);
     };
 
-    // Selector table: a constant copied into LDS while the first requests fly.
-    for (int e = threadIdx.x; e < 256; e += 64 * WPG) {
-        lut[e] = *(const u32x2 *)&kSelectors.v[2 * e];
-    }
-    if (nlt > 0) request(0);
+    request(0);
+    // Selector table, computed while the first requests fly.
+    for (int e = threadIdx.x; e < 256; e += 64 * WPG) lut[e] = perm_selectors((uint32_t)e);
     __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);                     // nothing that waits on the inputs moves above
 
-    auto process_chunk = [&](int c0) {
-        const int cnt = min(CH, nlt - c0);
+    // Chunk state shared by the staging and the decoding half.
+    int cnt = 0;
+    uint32_t A0 = 0;
+    __amdgpu_buffer_rsrc_t psrc;
+    i32x4 pf[C::kLoads];
+    auto load_piece = [&](int u) {
+        pf[u] = __builtin_amdgcn_raw_buffer_load_b128(psrc, (uint32_t)(16 * lane + 1024 * u), 0, kNonTemporal);
+    };
+
+    auto stage_chunk = [&](int c0) {
+        cnt = min(CH, nlt - c0);
         wait_vm_all();                                     // offsets, bitmaps, activations
 
         const uint32_t ob = lane_value(offv, 0), oe = lane_value(offv, cnt);
-        const uint32_t A0 = (ob >> 1) & ~15u;              // first staged payload byte
+        A0 = (ob >> 1) & ~15u;                             // first staged payload byte
         const uint32_t span = (((oe - 2u * A0) >> 3) << 2) + 8u;
         const uint32_t nq = min((span + 15u) >> 4, (uint32_t)C::kPayPieces);
         // Payload: 16-byte pieces from A0; load u brings stage bytes
@@ -317,13 +319,8 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
         // machine's requests and decoding starts while the rest streams.
         // Non-temporal: the stream does not displace the activations, which
         // every workgroup re-reads, from L2.
-        const __amdgpu_buffer_rsrc_t psrc = __builtin_amdgcn_make_buffer_rsrc(
+        psrc = __builtin_amdgcn_make_buffer_rsrc(
             (void *)(p.pay + A0), (short)0, (int)min(16u * nq, (uint32_t)p.pay_bytes - A0), kBufferDword3);
-        i32x4 pf[C::kLoads];
-        auto load_piece = [&](int u) {
-            pf[u] = __builtin_amdgcn_raw_buffer_load_b128(psrc, (uint32_t)(16 * lane + 1024 * u), 0,
-                                                          kNonTemporal);
-        };
         static_for<0, kWindow>([&](auto uc) {
             if constexpr (decltype(uc)::value < C::kLoads) load_piece(decltype(uc)::value);
         });
@@ -331,13 +328,12 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
         // Bitmaps (zero past the chunk), offsets and activations into the stage.
         if (lane < 2 * CH) lds_store4(st_bm + 16 * lane, lane < 2 * cnt ? pbm : (u32x4){0u, 0u, 0u, 0u});
         if (lane <= CH) lds_store(st_off + 4 * lane, offv);
-        if (x_piece < 2 * CH) {
 #pragma unroll
-            for (int u = 0; u < kXLoads; ++u)
-                if (u < x_loads)
-                    lds_store4(st_x + 4u * (uint32_t)((u * C::kXRows + x_slot) * C::kXRowWords) + 16 * x_piece,
-                               (u32x4)px[u]);
-        }
+        for (int u = 0; u < kXLoads; ++u)
+            if (u < x_loads && xs[u] != 0u) lds_store4(xs[u], (u32x4)px[u]);
+    };
+
+    auto decode_chunk = [&](int c0) {
 
         // Row bases: lanes 16 jj + rr handle LT j = 4 pass + jj, mask row i,
         // area row a. The scan over the 16 lanes of a DPP row starts area row
@@ -345,19 +341,28 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
         // popcounts of the rows before i.
         // LDS bit address of payload value v of the matrix: sbase + 4 v.
         const uint32_t sbase = 8u * st - 8u * A0;
+        {
+            const uint32_t jj = (uint32_t)lane >> 4;
+            const uint32_t p_bm = st_bm + 32 * jj + 4 * i, p_off = st_off + 4 * jj;
+            const uint32_t p_base = st_base + 64 * jj + 4 * rr, p_sd = st_sd + 4 * jj;
+            uint32_t mrow[C::kPasses];
+            uint2 o[C::kPasses];
 #pragma unroll
-        for (int ps = 0; ps < C::kPasses; ++ps) {
-            const int j = 4 * ps + (lane >> 4);
-            const uint32_t mrow = lds_load(st_bm + 4 * (8 * j + i));
-            const uint2 o = lds_load2(st_off + 4 * j);
-            const uint32_t rp = __popc(mrow);
-            const uint32_t inj = amask & ((o.y - o.x) >> 1);
-            uint32_t ex = (uint32_t)__builtin_amdgcn_update_dpp((int)inj, (int)rp, 0x112, 0xF, 0xF, false);
-            ex += dpp_row<0x112>(ex);
-            ex += dpp_row<0x114>(ex);
-            ex += dpp_row<0x118>(ex);
-            lds_store(st_base + 4 * (16 * j + rr), sbase + 4u * (o.x + ex));
-            if (rr == 0) lds_store(st_sd + 4 * j, o.y - o.x);
+            for (int ps = 0; ps < C::kPasses; ++ps) {
+                mrow[ps] = lds_load(p_bm + 128 * ps);
+                o[ps] = lds_load2(p_off + 16 * ps);
+            }
+#pragma unroll
+            for (int ps = 0; ps < C::kPasses; ++ps) {
+                const uint32_t inj = amask & ((o[ps].y - o[ps].x) >> 1);
+                uint32_t ex = (uint32_t)__builtin_amdgcn_update_dpp((int)inj, (int)__popc(mrow[ps]), 0x112, 0xF,
+                                                                    0xF, false);
+                ex += dpp_row<0x112>(ex);
+                ex += dpp_row<0x114>(ex);
+                ex += dpp_row<0x118>(ex);
+                lds_store(p_base + 256 * ps, sbase + 4u * (o[ps].x + ex));
+                if (rr == 0) lds_store(p_sd + 16 * ps, o[ps].y - o[ps].x);
+            }
         }
         // LT k can be decoded once the pieces holding its windows have landed:
         // o_{k+1} - 2 A0 + 16 <= 2048 (u + 1), i.e. after load u = need_k.
@@ -423,8 +428,14 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
     };
     // The first chunk is straight-line code after the prologue, so every
     // wait above counts loads exactly; later chunks only occur for long slices.
-    if (nlt > 0) process_chunk(0);
-    for (int c0 = CH; c0 < nlt; c0 += CH) process_chunk(c0);
+    // Every slice holds at least one LT (the host never splits K into more
+    // slices than LTs), so the first chunk needs no branch.
+    stage_chunk(0);
+    decode_chunk(0);
+    for (int c0 = CH; c0 < nlt; c0 += CH) {
+        stage_chunk(c0);
+        decode_chunk(c0);
+    }
 
     // Split-K combine: each wavefront leaves its 16 x (16 NB) partial in its
     // own stage, in MFMA result layout (lane l, element v: row 4 (l / 16) + v,
@@ -570,6 +581,7 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
         if (s != 0) {
             if (s != 1 && s != 2 && s != 4 && s != 8 && s != 16) return US_ERR_ARG;
             wpg = s;
+            while (wpg > nkb) wpg /= 2;                    // at least one LT per slice
             ch = pick_chunk((int)nkb, N, wpg);
         }
     }
