@@ -213,7 +213,9 @@ __device__ __forceinline__ i32x4 unpack_x(uint2 x) {
                    (int32_t)((x.y << 4) & kHiNib), (int32_t)(x.y & kHiNib)};
 }
 
-template <int WPG, int NB, int CH>
+// MULTI: some slices take several chunks (their inputs are then requested
+// one chunk ahead); otherwise every slice is a single chunk.
+template <int WPG, int NB, int CH, bool MULTI>
 __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage_bytes) {
     using C = Chunk<CH>;
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
@@ -280,7 +282,7 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
     u32x4 pbm;
     i32x4 px[kXLoads];
     auto request = [&](int c0) {
-        const int cnt = max(1, min(CH, nlt - c0));         // clamped: a slice may be empty
+        const int cnt = min(CH, nlt - c0);                 // >= 1
         offv = p.off[t0 + c0 + min(lane, cnt)];
         pbm = *(const u32x4 *)(p.bm32 + 8 * (t0 + c0) + 4 * min(lane, 2 * cnt - 1));
         const uint32_t xk = (uint32_t)(32 * (kb0 + c0));
@@ -321,16 +323,30 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
         // every workgroup re-reads, from L2.
         psrc = __builtin_amdgcn_make_buffer_rsrc(
             (void *)(p.pay + A0), (short)0, (int)min(16u * nq, (uint32_t)p.pay_bytes - A0), kBufferDword3);
-        static_for<0, kWindow>([&](auto uc) {
-            if constexpr (decltype(uc)::value < C::kLoads) load_piece(decltype(uc)::value);
-        });
-
+        auto issue_window = [&]() {
+            static_for<0, kWindow>([&](auto uc) {
+                if constexpr (decltype(uc)::value < C::kLoads) load_piece(decltype(uc)::value);
+            });
+        };
         // Bitmaps (zero past the chunk), offsets and activations into the stage.
-        if (lane < 2 * CH) lds_store4(st_bm + 16 * lane, lane < 2 * cnt ? pbm : (u32x4){0u, 0u, 0u, 0u});
-        if (lane <= CH) lds_store(st_off + 4 * lane, offv);
+        auto commit_inputs = [&]() {
+            if (lane < 2 * CH) lds_store4(st_bm + 16 * lane, lane < 2 * cnt ? pbm : (u32x4){0u, 0u, 0u, 0u});
+            if (lane <= CH) lds_store(st_off + 4 * lane, offv);
 #pragma unroll
-        for (int u = 0; u < kXLoads; ++u)
-            if (u < x_loads && xs[u] != 0u) lds_store4(xs[u], (u32x4)px[u]);
+            for (int u = 0; u < kXLoads; ++u)
+                if (u < x_loads && xs[u] != 0u) lds_store4(xs[u], (u32x4)px[u]);
+        };
+        if (MULTI && nlt - c0 > CH) {
+            // A later chunk follows: once this chunk's inputs are in LDS their
+            // registers take the next chunk's inputs, requested ahead of this
+            // chunk's payload so that the payload waits below cover them.
+            commit_inputs();
+            request(c0 + CH);
+            issue_window();
+        } else {
+            issue_window();
+            commit_inputs();
+        }
     };
 
     auto decode_chunk = [&](int c0) {
@@ -422,9 +438,6 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
             }
         });
         __asm__ volatile("" ::: "memory");
-
-        // Next chunk (long slices only).
-        if (nlt - c0 - CH > 0) request(c0 + CH);
     };
     // The first chunk is straight-line code after the prologue, so every
     // wait above counts loads exactly; later chunks only occur for long slices.
@@ -432,9 +445,11 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
     // slices than LTs), so the first chunk needs no branch.
     stage_chunk(0);
     decode_chunk(0);
-    for (int c0 = CH; c0 < nlt; c0 += CH) {
-        stage_chunk(c0);
-        decode_chunk(c0);
+    if constexpr (MULTI) {
+        for (int c0 = CH; c0 < nlt; c0 += CH) {
+            stage_chunk(c0);
+            decode_chunk(c0);
+        }
     }
 
     // Split-K combine: each wavefront leaves its 16 x (16 NB) partial in its
@@ -473,10 +488,14 @@ int lds_bytes(int ch, int N, int wpg) {
 
 template <int WPG, int NB, int CH>
 hipError_t launch_spmm(const SpmmArgs &a, hipStream_t s) {
-    auto kern = us_spmm_kernel<WPG, NB, CH>;
+    const bool multi = (a.nkb + WPG - 1) / WPG > CH;
+    auto kern = multi ? us_spmm_kernel<WPG, NB, CH, true> : us_spmm_kernel<WPG, NB, CH, false>;
     // Allow more than 64 KB of dynamic LDS (set once per instantiation).
     static const hipError_t attr =
-        hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes);
+        (hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, true>,
+                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes),
+         hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, false>,
+                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes));
     (void)attr;
     const int st = stage_bytes<CH>(a.N);
     hipLaunchKernelGGL(kern, dim3(a.M / 16), dim3(64 * WPG), WPG * st, s, a, st);
