@@ -45,6 +45,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "us.h"
@@ -541,24 +542,48 @@ int pick_chunk(int nkb, int N, int wpg) {
     return best;
 }
 
-// Wavefronts per workgroup (= K slices per row block): at least 16 wavefronts
-// per CU over 256 CUs, one chunk per slice where 16 slices allow it, at least
-// one LT per slice, and an LDS footprint that fits.
-void auto_config(int M, int K, int N, int &wpg, int &ch) {
+// Wavefronts per workgroup (= K slices per row block). A wavefront pays one
+// memory round trip (offsets, then payload) per chunk, and a CU runs one
+// generation of resident workgroups after another, so the choice minimises
+// the number of such latency-bound phases: generations x chunks per slice.
+// Ties go to fewer chunks per slice, then to more wavefronts per CU.
+// Residency: LDS, and at most 16 wavefronts per CU (the kernel's registers).
+void auto_config(int M, int K, int N, int n_cu, int &wpg, int &ch) {
     const int nrb = M / 16, nkb = K / 64;
-    int w = 1;
-    while (w < 16 && nrb * w < 256 * 16) w *= 2;
-    while (w > 1 && w > nkb) w /= 2;
-    wpg = w;
-    ch = pick_chunk(nkb, N, w);
-    // Widen while a slice still needs several chunks and a wider split fits.
-    while (w < 16 && 2 * w <= nkb && ch < (nkb + w - 1) / w) {
-        w *= 2;
+    long best[3] = {0, 0, 0};
+    wpg = 0;
+    ch = 0;
+    for (int w = 16; w >= 1; w /= 2) {
+        if (w > nkb) continue;
         const int c = pick_chunk(nkb, N, w);
-        if (lds_bytes(c, N, w) > kMaxLds) break;
-        wpg = w;
-        ch = c;
+        if (c == 0) continue;
+        const int lds = lds_bytes(c, N, w);
+        if (lds > kMaxLds) continue;
+        const int per_cu = max(1, min(kMaxLds / lds, 16 / w));          // resident workgroups per CU
+        const long gens = (nrb + (long)n_cu * per_cu - 1) / ((long)n_cu * per_cu);
+        const long chunks = ((nkb + w - 1) / w + c - 1) / c;
+        const long waves = (long)w * min((long)per_cu, (nrb + n_cu - 1) / (long)n_cu);
+        const long key[3] = {gens * chunks, chunks, -waves};
+        if (wpg == 0 || key[0] < best[0] || (key[0] == best[0] && (key[1] < best[1] ||
+                                                                   (key[1] == best[1] && key[2] < best[2])))) {
+            for (int k = 0; k < 3; ++k) best[k] = key[k];
+            wpg = w;
+            ch = c;
+        }
     }
+}
+
+// Compute units of the current device (queried once per device).
+int device_cus() {
+    static std::atomic<int> cached[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int n = cached[dev].load(std::memory_order_relaxed);
+    if (n <= 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cached[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
 }
 
 }  // namespace
@@ -593,7 +618,7 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
         return US_ERR_ARG;
 
     int wpg = 0, ch = 0;
-    auto_config(M, K, N, wpg, ch);
+    auto_config(M, K, N, device_cus(), wpg, ch);
     if (opts) {
         if (opts->variant != 0) return US_ERR_ARG;
         const int s = opts->split_k;
