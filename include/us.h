@@ -126,7 +126,9 @@ typedef struct {
     int32_t split_k;  /* K slices per 16-row block, one wavefront each:
                          0 = automatic, else 1, 2, 4, 8 or 16; halved
                          while it exceeds K / 64 (one LT per slice)      */
-    int32_t variant;  /* reserved, must be 0                             */
+    int32_t variant;  /* payload staging in LDS: 0 = automatic, 1 = whole
+                         chunk, 2 = 4 KB ring (N <= 16 only); a choice
+                         that fits no configuration returns US_ERR_ARG   */
 } us_spmm_opts;
 
 /*

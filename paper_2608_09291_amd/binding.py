@@ -229,10 +229,10 @@ def workspace_size(M: int, K: int, N: int, split_k: int = 0) -> int:
 
 
 def spmm(w: DeviceEncoded, x_packed, N: int, y, scale=None, y_f32=None, split_k: int = 0,
-         ws=None, stream=None, wstruct: IEBMEDev = None) -> None:
+         ws=None, stream=None, wstruct: IEBMEDev = None, variant: int = 0) -> None:
     """us_spmm: y[n, m] = sum_k W[m, k] X[k, n] (+ optional dequant into y_f32)."""
     s = wstruct if wstruct is not None else w.struct()
-    opts = SpmmOpts(split_k, 0)
+    opts = SpmmOpts(split_k, variant)
     _check("us_spmm", lib().us_spmm(
         ctypes.byref(s), x_packed.data_ptr(), N, y.data_ptr(),
         None if scale is None else scale.data_ptr(),

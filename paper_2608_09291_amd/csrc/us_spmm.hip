@@ -91,28 +91,39 @@ __device__ u32x2 perm_selectors(uint32_t m) {
 }
 
 // LDS stage of one chunk of CH LTs (per wavefront), in bytes from the stage start:
-//   payload : the chunk's compressed values. The stage starts at the 16-byte
+//   payload : the chunk's compressed values, streamed from the 16-byte
 //             boundary at or below the chunk's first byte (up to 15 bytes
-//             early) and a segment window may read 8 bytes past the last
-//             value, so at most 32 CH + 2 pieces of 16 bytes are staged;
+//             early); a segment window may read 8 bytes past the last value,
+//             so a chunk needs at most 32 CH + 2 pieces of 16 bytes.
+//             Linear staging (RING = false) keeps the whole chunk. RING =
+//             true keeps a ring of four 1 KB slots (stream byte b in slot
+//             (b / 1024) mod 4), so the stage does not grow with CH: an LT
+//             spans at most 528 bytes with its window overhang, so the four
+//             slots hold every LT that is ready for decoding. The 160 bytes
+//             after the ring repeat its first 160 bytes, so windows that start
+//             past the end of the ring (by at most one stream, 128 bytes,
+//             plus a window) read on into it;
 //   bitmaps : union-mask rows, 8 dwords per LT;
 //             (this and the next three arrays have room for a whole number
 //             of 4-LT passes; entries past the chunk are never decoded)
 //   bases   : per LT and lane row rr = 2i + a, the LDS bit address of the
-//             first value of row i in area stream 2a (16 dwords per LT);
+//             first value of row i in area stream 2a (folded into the ring
+//             with RING; 16 dwords per LT);
 //   sd      : per LT, the number of bits of one area stream (o_{t+1} - o_t);
 //   offsets : o_t of the chunk's LTs and the end offset (CH + 1 dwords);
 //   X       : the chunk's activation slice, one row of 32 bytes per LT for
 //             each activation column; rows are 16 bytes longer than the
 //             slice so that the 16 rows read by one instruction fall in
 //             different LDS banks.
-template <int CH>
+template <int CH, bool RING>
 struct Chunk {
     static constexpr int kPayPieces = 32 * CH + 2;
     static constexpr int kLoads = (kPayPieces + 63) / 64;     // payload loads per lane
+    static constexpr int kRing = 4096;                        // ring: four 1 KB slots
+    static constexpr int kGuard = 160;                        // copy of the ring's first bytes
     static constexpr int kPasses = (CH + 3) / 4;              // base passes, 4 LTs each
     static constexpr int kLtPad = 4 * kPasses;                // per-LT arrays padded to whole passes
-    static constexpr int kBmOffset = 16 * kPayPieces;
+    static constexpr int kBmOffset = RING ? kRing + kGuard : 16 * kPayPieces;
     static constexpr int kBaseOffset = kBmOffset + 32 * kLtPad;
     static constexpr int kSdOffset = kBaseOffset + 64 * kLtPad;
     static constexpr int kOffOffset = kSdOffset + 4 * kLtPad;
@@ -215,10 +226,11 @@ __device__ __forceinline__ i32x4 unpack_x(uint2 x) {
 }
 
 // MULTI: some slices take several chunks (their inputs are then requested
-// one chunk ahead); otherwise every slice is a single chunk.
-template <int WPG, int NB, int CH, bool MULTI>
+// one chunk ahead); otherwise every slice is a single chunk. RING: the
+// payload is staged in a 4 KB ring instead of whole (see Chunk).
+template <int WPG, int NB, int CH, bool MULTI, bool RING>
 __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage_bytes) {
-    using C = Chunk<CH>;
+    using C = Chunk<CH, RING>;
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
     __shared__ u32x2 lut[256];                               // selector table
     const uint32_t lds0 = (uint32_t)(size_t)(lds_u32 *)lds;  // LDS address of the dynamic block
@@ -356,8 +368,9 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
         // area row a. The scan over the 16 lanes of a DPP row starts area row
         // a = 1 at 2 P_t (its streams follow streams 0 and 1) and adds the
         // popcounts of the rows before i.
-        // LDS bit address of payload value v of the matrix: sbase + 4 v.
-        const uint32_t sbase = 8u * st - 8u * A0;
+        // Payload value v of the matrix is stream bit 4 v - 8 A0, at LDS bit
+        // address 8 st + (4 v - 8 A0), taken mod 32768 with the ring.
+        const uint32_t rmask = RING ? 0x7FFFu : ~0u;
         {
             const uint32_t jj = (uint32_t)lane >> 4;
             const uint32_t p_bm = st_bm + 32 * jj + 4 * i, p_off = st_off + 4 * jj;
@@ -377,7 +390,7 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
                 ex += dpp_row<0x112>(ex);
                 ex += dpp_row<0x114>(ex);
                 ex += dpp_row<0x118>(ex);
-                lds_store(p_base + 256 * ps, sbase + 4u * (o[ps].x + ex));
+                lds_store(p_base + 256 * ps, 8u * st + ((4u * (o[ps].x + ex) - 8u * A0) & rmask));
                 if (rr == 0) lds_store(p_sd + 16 * ps, o[ps].y - o[ps].x);
             }
         }
@@ -400,8 +413,13 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
             const uint32_t sd = lds_load(a_sd);
             const i32x4 A = decode_tile(lut, mrow, base, sd, lomask, rot);
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
+            for (int nb = 0; nb < NB; ++nb) {
                 acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, unpack_x(x_pair(a_x[nb])), acc[nb], 0, 0, 0);
+                a_x[nb] += 32;
+            }
+            a_bm += 32;
+            a_base += 64;
+            a_sd += 4;
         };
         auto decode_two = [&]() {
             const uint32_t m0 = lds_load(a_bm), m1 = lds_load(a_bm + 32);
@@ -420,19 +438,33 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
             a_sd += 8;
         };
 
-        // The payload lands in issue order: after load u, stage bytes
-        // [0, 1024 (u + 1)) are present, so LTs with need <= u can be decoded.
+        // The payload lands in issue order: after load u, stream bytes
+        // [0, 1024 (u + 1)) have arrived (and, with the ring, bytes from
+        // 1024 (u - 3) on are still held), so LTs with need <= u can be
+        // decoded. LTs go in pairs; one that waits for its partner waits one
+        // step at most (the partner spans at most 528 more bytes). With the
+        // ring the chunk's last LT goes alone as soon as it is ready, as
+        // later steps may refill its slots.
         int j = 0;
         static_for<0, C::kLoads>([&](auto uc) {
             constexpr int u = decltype(uc)::value;
             constexpr int later = (kWindow - 1 < C::kLoads - 1 - u) ? kWindow - 1 : C::kLoads - 1 - u;
             wait_vm<later>();                              // piece u has landed
             if constexpr (u + kWindow < C::kLoads) load_piece(u + kWindow);
-            if (u + 1 < C::kLoads || lane + 64 * u < C::kPayPieces) lds_store4(st + 1024 * u + 16 * lane, (u32x4)pf[u]);
+            if constexpr (RING) {
+                lds_store4(st + 1024 * (u & 3) + 16 * lane, (u32x4)pf[u]);
+                if ((u & 3) == 0 && lane < C::kGuard / 16) lds_store4(st + C::kRing + 16 * lane, (u32x4)pf[u]);
+            } else if (u + 1 < C::kLoads || lane + 64 * u < C::kPayPieces) {
+                lds_store4(st + 1024 * u + 16 * lane, (u32x4)pf[u]);
+            }
             __asm__ volatile("" ::: "memory");
             if constexpr (u + 1 < C::kLoads) {
                 const int ready = __builtin_popcountll(__builtin_amdgcn_ballot_w64(lane < cnt && need <= (uint32_t)u));
                 for (; j + 1 < ready; j += 2) decode_two();
+                if (RING && j < ready && ready == cnt) {
+                    decode_one();
+                    ++j;
+                }
             } else {
                 for (; j + 1 < cnt; j += 2) decode_two();
                 if (j < cnt) decode_one();
@@ -476,99 +508,116 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
     }
 }
 
-template <int CH>
-int stage_bytes(int N) { return (Chunk<CH>::bytes(N) + 15) & ~15; }
+// Chunk configurations: chunk length and payload staging (see Chunk).
+// Two MFMA column blocks (N > 16) use the short linear ones only.
+struct ChunkCfg {
+    int ch;
+    bool ring;
+};
+constexpr ChunkCfg kCfgs[] = {{4, false}, {8, false}, {11, false}, {16, false}, {16, true}};
+constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
-int lds_bytes(int ch, int N, int wpg) {
-    const int st = ch == 16 ? stage_bytes<16>(N)
-                 : ch == 11 ? stage_bytes<11>(N)
-                 : ch == 8  ? stage_bytes<8>(N)
-                            : stage_bytes<4>(N);
+bool cfg_allowed(int idx, int N) { return N <= 16 || (kCfgs[idx].ch <= 8 && !kCfgs[idx].ring); }
+
+template <int CH, bool RING>
+int stage_bytes(int N) { return (Chunk<CH, RING>::bytes(N) + 15) & ~15; }
+
+int lds_bytes(int idx, int N, int wpg) {
+    int st = 0;
+    switch (idx) {
+        case 0: st = stage_bytes<4, false>(N); break;
+        case 1: st = stage_bytes<8, false>(N); break;
+        case 2: st = stage_bytes<11, false>(N); break;
+        case 3: st = stage_bytes<16, false>(N); break;
+        default: st = stage_bytes<16, true>(N); break;
+    }
     return kLutBytes + wpg * st;
 }
 
-template <int WPG, int NB, int CH>
+template <int WPG, int NB, int CH, bool RING>
 hipError_t launch_spmm(const SpmmArgs &a, hipStream_t s) {
     const bool multi = (a.nkb + WPG - 1) / WPG > CH;
-    auto kern = multi ? us_spmm_kernel<WPG, NB, CH, true> : us_spmm_kernel<WPG, NB, CH, false>;
+    auto kern = multi ? us_spmm_kernel<WPG, NB, CH, true, RING> : us_spmm_kernel<WPG, NB, CH, false, RING>;
     // Allow more than 64 KB of dynamic LDS (set once per instantiation).
     static const hipError_t attr =
-        (hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, true>,
+        (hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, true, RING>,
                              hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes),
-         hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, false>,
+         hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, false, RING>,
                              hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes));
     (void)attr;
-    const int st = stage_bytes<CH>(a.N);
+    const int st = stage_bytes<CH, RING>(a.N);
     hipLaunchKernelGGL(kern, dim3(a.M / 16), dim3(64 * WPG), WPG * st, s, a, st);
     return hipGetLastError();
 }
 
-template <int NB, int CH>
+template <int NB, int CH, bool RING>
 hipError_t launch_spmm_wpg(int wpg, const SpmmArgs &a, hipStream_t s) {
     switch (wpg) {
-        case 1: return launch_spmm<1, NB, CH>(a, s);
-        case 2: return launch_spmm<2, NB, CH>(a, s);
-        case 4: return launch_spmm<4, NB, CH>(a, s);
-        case 8: return launch_spmm<8, NB, CH>(a, s);
-        default: return launch_spmm<16, NB, CH>(a, s);
+        case 1: return launch_spmm<1, NB, CH, RING>(a, s);
+        case 2: return launch_spmm<2, NB, CH, RING>(a, s);
+        case 4: return launch_spmm<4, NB, CH, RING>(a, s);
+        case 8: return launch_spmm<8, NB, CH, RING>(a, s);
+        default: return launch_spmm<16, NB, CH, RING>(a, s);
     }
 }
 
-hipError_t launch_cfg(int wpg, int ch, const SpmmArgs &a, hipStream_t s) {
-    if (a.N > 16) return ch == 8 ? launch_spmm_wpg<2, 8>(wpg, a, s) : launch_spmm_wpg<2, 4>(wpg, a, s);
-    switch (ch) {
-        case 16: return launch_spmm_wpg<1, 16>(wpg, a, s);
-        case 11: return launch_spmm_wpg<1, 11>(wpg, a, s);
-        case 8: return launch_spmm_wpg<1, 8>(wpg, a, s);
-        default: return launch_spmm_wpg<1, 4>(wpg, a, s);
+hipError_t launch_cfg(int wpg, int idx, const SpmmArgs &a, hipStream_t s) {
+    if (a.N > 16) return idx == 1 ? launch_spmm_wpg<2, 8, false>(wpg, a, s) : launch_spmm_wpg<2, 4, false>(wpg, a, s);
+    switch (idx) {
+        case 4: return launch_spmm_wpg<1, 16, true>(wpg, a, s);
+        case 3: return launch_spmm_wpg<1, 16, false>(wpg, a, s);
+        case 2: return launch_spmm_wpg<1, 11, false>(wpg, a, s);
+        case 1: return launch_spmm_wpg<1, 8, false>(wpg, a, s);
+        default: return launch_spmm_wpg<1, 4, false>(wpg, a, s);
     }
 }
 
 bool aligned(const void *ptr, uintptr_t n) { return ((uintptr_t)ptr % n) == 0; }
 
-// Chunk length for wpg slices: the smallest of 4, 8, 11, 16 LTs (4 or 8 with
-// two MFMA column blocks) that holds a whole slice and fits LDS; else the
-// largest that fits (the slice then takes several chunks). 4 always fits.
-int pick_chunk(int nkb, int N, int wpg) {
-    const int slice = (nkb + wpg - 1) / wpg;
-    const int cands[4] = {4, 8, 11, 16};
-    const int nc = N > 16 ? 2 : 4;
-    int best = 0;
-    for (int c = 0; c < nc; ++c) {
-        if (lds_bytes(cands[c], N, wpg) > kMaxLds) break;
-        best = cands[c];
-        if (cands[c] >= slice) return best;
-    }
-    return best;
-}
-
-// Wavefronts per workgroup (= K slices per row block). A wavefront pays one
-// memory round trip (offsets, then payload) per chunk, and a CU runs one
-// generation of resident workgroups after another, so the choice minimises
-// the number of such latency-bound phases: generations x chunks per slice.
-// Ties go to fewer chunks per slice, then to more wavefronts per CU.
-// Residency: LDS, and at most 16 wavefronts per CU (the kernel's registers).
-void auto_config(int M, int K, int N, int n_cu, int &wpg, int &ch) {
+// Wavefronts per workgroup (= K slices per row block) and chunk
+// configuration. A wavefront pays one memory round trip (offsets, then
+// payload) per chunk, and a CU runs one generation of resident workgroups
+// after another, so the choice minimises the number of such latency-bound
+// phases: generations x chunks per slice. Ties go to fewer generations (a
+// wavefront requests its next chunk's inputs early; a new workgroup starts
+// cold), then to more wavefronts per CU, then to linear staging and shorter
+// chunks. Residency: LDS, and at most 16 wavefronts per CU (the kernel's
+// registers). wpg_only > 0 fixes the number of wavefronts; staging 1 or 2
+// allows linear or ring payload staging only (0: either).
+void choose_config(int M, int K, int N, int n_cu, int wpg_only, int staging, int &wpg, int &cfg) {
     const int nrb = M / 16, nkb = K / 64;
-    long best[3] = {0, 0, 0};
+    long best[5] = {0, 0, 0, 0, 0};
     wpg = 0;
-    ch = 0;
+    cfg = -1;
+    // With two column blocks every chunk stages 32 activation rows, so
+    // short slices pay that per few LTs: at most 4 slices per row block
+    // (measured on 12288 x 4096 and 28672 x 8192 at N = 32).
+    const int w_max = N > 16 ? 4 : 16;
     for (int w = 16; w >= 1; w /= 2) {
-        if (w > nkb) continue;
-        const int c = pick_chunk(nkb, N, w);
-        if (c == 0) continue;
-        const int lds = lds_bytes(c, N, w);
-        if (lds > kMaxLds) continue;
-        const int per_cu = max(1, min(kMaxLds / lds, 16 / w));          // resident workgroups per CU
-        const long gens = (nrb + (long)n_cu * per_cu - 1) / ((long)n_cu * per_cu);
-        const long chunks = ((nkb + w - 1) / w + c - 1) / c;
-        const long waves = (long)w * min((long)per_cu, (nrb + n_cu - 1) / (long)n_cu);
-        const long key[3] = {gens * chunks, chunks, -waves};
-        if (wpg == 0 || key[0] < best[0] || (key[0] == best[0] && (key[1] < best[1] ||
-                                                                   (key[1] == best[1] && key[2] < best[2])))) {
-            for (int k = 0; k < 3; ++k) best[k] = key[k];
-            wpg = w;
-            ch = c;
+        if (w > nkb || (wpg_only > 0 && w != wpg_only) || (wpg_only == 0 && w > w_max)) continue;
+        for (int idx = 0; idx < kNumCfgs; ++idx) {
+            if (!cfg_allowed(idx, N) || (staging == 1 && kCfgs[idx].ring) || (staging == 2 && !kCfgs[idx].ring))
+                continue;
+            const int lds = lds_bytes(idx, N, w);
+            if (lds > kMaxLds) continue;
+            const int c = kCfgs[idx].ch;
+            const int per_cu = max(1, min(kMaxLds / lds, 16 / w));      // resident workgroups per CU
+            const long gens = (nrb + (long)n_cu * per_cu - 1) / ((long)n_cu * per_cu);
+            const long chunks = ((nkb + w - 1) / w + c - 1) / c;
+            const long waves = (long)w * min((long)per_cu, (nrb + n_cu - 1) / (long)n_cu);
+            const long key[5] = {gens * chunks, gens, -waves, kCfgs[idx].ring ? 1 : 0, c};
+            bool better = cfg < 0;
+            for (int k = 0; k < 5 && !better; ++k) {
+                if (key[k] != best[k]) {
+                    better = key[k] < best[k];
+                    break;
+                }
+            }
+            if (better) {
+                for (int k = 0; k < 5; ++k) best[k] = key[k];
+                wpg = w;
+                cfg = idx;
+            }
         }
     }
 }
@@ -593,7 +642,7 @@ extern "C" us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, con
     if (!bytes) return US_ERR_ARG;
     if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
     if (N < 1 || N > US_N_MAX) return US_ERR_SHAPE;
-    if (opts && (opts->variant != 0 || opts->split_k < 0)) return US_ERR_ARG;
+    if (opts && (opts->variant < 0 || opts->variant > 2 || opts->split_k < 0)) return US_ERR_ARG;
     *bytes = 0;
     return US_OK;
 }
@@ -617,19 +666,20 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
         (scale && (!aligned(scale, 4) || !aligned(y_f32, 4))))
         return US_ERR_ARG;
 
-    int wpg = 0, ch = 0;
-    auto_config(M, K, N, device_cus(), wpg, ch);
+    int wpg_only = 0, staging = 0;
     if (opts) {
-        if (opts->variant != 0) return US_ERR_ARG;
+        if (opts->variant < 0 || opts->variant > 2) return US_ERR_ARG;
+        staging = opts->variant;
         const int s = opts->split_k;
         if (s != 0) {
             if (s != 1 && s != 2 && s != 4 && s != 8 && s != 16) return US_ERR_ARG;
-            wpg = s;
-            while (wpg > nkb) wpg /= 2;                    // at least one LT per slice
-            ch = pick_chunk((int)nkb, N, wpg);
+            wpg_only = s;
+            while (wpg_only > nkb) wpg_only /= 2;          // at least one LT per slice
         }
     }
-    if (ch == 0) return US_ERR_ARG;                        // no chunk fits LDS
+    int wpg = 0, cfg = -1;
+    choose_config(M, K, N, device_cus(), wpg_only, staging, wpg, cfg);
+    if (cfg < 0) return US_ERR_ARG;                        // no configuration fits LDS
 
     SpmmArgs a;
     a.bm32 = (const uint32_t *)w->bitmaps;
@@ -649,6 +699,6 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     a.nkb = (int32_t)nkb;
 
     hipStream_t s = (hipStream_t)stream;
-    const hipError_t err = launch_cfg(wpg, ch, a, s);
+    const hipError_t err = launch_cfg(wpg, cfg, a, s);
     return err == hipSuccess ? US_OK : US_ERR_DEVICE;
 }

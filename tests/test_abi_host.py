@@ -200,7 +200,7 @@ def test_spmm_argument_errors_before_launch(case, status):
     elif case == "split_3":
         opts.split_k = 3
     elif case == "variant":
-        opts.variant = 1
+        opts.variant = 3
     elif case == "misaligned_x":
         x = 0x2002
     got = L.us_spmm(wp, x, N, y, sc, yf, None, 0, ctypes.byref(opts), None)

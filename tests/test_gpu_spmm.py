@@ -32,7 +32,7 @@ def announce(msg):
     sys.stderr.flush()
 
 
-def run_spmm(torch, W, Xt, scale=None, split_k=0, dev=None):
+def run_spmm(torch, W, Xt, scale=None, split_k=0, dev=None, variant=0):
     M, K = W.shape
     N = Xt.shape[0]
     if dev is None:
@@ -43,7 +43,7 @@ def run_spmm(torch, W, Xt, scale=None, split_k=0, dev=None):
     if scale is not None:
         sc = torch.from_numpy(np.asarray(scale, dtype=np.float32)).cuda()
         yf = torch.full((N, M), float("nan"), dtype=torch.float32, device="cuda")
-    binding.spmm(dev, xp, N, y, sc, yf, split_k=split_k)
+    binding.spmm(dev, xp, N, y, sc, yf, split_k=split_k, variant=variant)
     torch.cuda.synchronize()
     Y = y.cpu().numpy().T
     Yf = None if yf is None else yf.cpu().numpy().T
@@ -98,6 +98,30 @@ def test_every_split(torch_cuda, split_k, N):
     dev = binding.to_device(binding.encode(W))
     Y, Yf = run_spmm(torch_cuda, W, Xt, sc, split_k=split_k, dev=dev)
     check(Y, Yf, W, Xt, sc)
+
+
+# Forced payload staging: whole chunks (1) and the 4 KB ring (2). Slices of
+# 19, 37 and 74 LTs take one or more chunks with an odd last chunk; at
+# s = 0.3 an LT nearly fills its 512 bytes, so the ring wraps inside LTs.
+@pytest.mark.parametrize("variant", [1, 2])
+@pytest.mark.parametrize("M,K,N,s,split_k", [
+    (32, 2368, 8, 0.5, 2),       # 37 LTs per row block
+    (32, 2368, 1, 0.3, 1),
+    (48, 4736, 16, 0.5, 1),      # 74 LTs, five chunks of up to 16
+    (64, 1216, 4, 0.0, 1),       # 19 LTs, every group active
+])
+def test_staging_variants(torch_cuda, variant, M, K, N, s, split_k):
+    announce(f"staging variant={variant} M={M} K={K} N={N} s={s} split={split_k}")
+    W, Xt, sc = synth.random_problem(M, K, N, s, 300 + 7 * variant + split_k)
+    Y, Yf = run_spmm(torch_cuda, W, Xt, sc, split_k=split_k, variant=variant)
+    check(Y, Yf, W, Xt, sc)
+
+
+def test_ring_refused_for_two_column_blocks(torch_cuda):
+    announce("ring variant with N=32 is refused")
+    W, Xt, _ = synth.random_problem(32, 1024, 32, 0.5, 17)
+    with pytest.raises(binding.UsError):
+        run_spmm(torch_cuda, W, Xt, variant=2)
 
 
 def test_row_skewed_density(torch_cuda):
