@@ -305,6 +305,11 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
     };
 
     request(0);
+    // The dequant scale of the output row this thread stores in the epilogue
+    // (outputs e = threadIdx.x + 64 WPG k all have row e mod 16), requested
+    // now so that the epilogue does not wait for it.
+    float row_scale = 0.0f;
+    if (p.scale && (int)threadIdx.x < 16 * N) row_scale = p.scale[(int64_t)mb * 16 + (threadIdx.x & 15)];
     // Selector table, computed while the first requests fly.
     for (int e = threadIdx.x; e < 256; e += 64 * WPG) lut[e] = perm_selectors((uint32_t)e);
     __syncthreads();
@@ -504,7 +509,7 @@ __global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage
         const int64_t m = (int64_t)mb * 16 + r;
         const int64_t M = p.M;
         p.y[n * M + m] = yv;
-        if (p.scale) p.yf[n * M + m] = (float)yv * p.scale[m];
+        if (p.scale) p.yf[n * M + m] = (float)yv * row_scale;
     }
 }
 
