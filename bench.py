@@ -282,6 +282,7 @@ def main():
         log(f"[bench] cpu oracle {cpu['ms_per_call']} ms/call on {cpu['cores']} threads")
 
     rep = r["rep"]
+    plan = binding.spmm_plan(w.M, w.K, N, args.split_k)
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -296,7 +297,8 @@ def main():
         "dtype": "int8",
         "data": "synthetic",
         "config": {"workload": w.name, "M": w.M, "K": w.K, "N": N, "sparsity": w.sparsity,
-                   "dequant": w.dequant, "split_k": args.split_k or "auto",
+                   "dequant": w.dequant, "split_k": plan[0], "chunk_lts": plan[1],
+                   "staging": "ring" if plan[2] == 2 else "whole", "plan": "auto" if not args.split_k else "forced",
                    "weights": "w4a4 IE-BME (16x64 tiles, 2x2 areas), int8 MFMA, int32 accumulate",
                    "rotating_copies": r["n_copies"]},
         "us_per_call": round(us, 3),

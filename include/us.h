@@ -132,6 +132,17 @@ typedef struct {
 } us_spmm_opts;
 
 /*
+ * us_spmm_plan - the launch configuration us_spmm would use for this shape
+ * and options on the current device (a 256-CU MI355X when no device is
+ * visible): K slices per 16-row block (one wavefront each), LTs per chunk,
+ * and payload staging (1 whole chunk, 2 ring). Host only; for tuning and
+ * reporting. Same argument errors as us_spmm; US_ERR_ARG if no
+ * configuration fits.
+ */
+us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, const us_spmm_opts *opts, int32_t *split_k,
+                       int32_t *chunk_lts, int32_t *staging);
+
+/*
  * us_spmm_workspace_size - device workspace bytes us_spmm needs for this
  * shape and options (0 today: the split-K sums are combined on chip).
  */

@@ -24,7 +24,7 @@ N_MAX = 32
 K_MAX = 130048
 
 #: Every symbol the two public headers declare.
-EXPORTS = ("us_encode", "us_iebme_free", "us_pmr", "us_spmm_workspace_size", "us_spmm",
+EXPORTS = ("us_encode", "us_iebme_free", "us_pmr", "us_spmm_plan", "us_spmm_workspace_size", "us_spmm",
            "us_gemm_i8", "us_status_string", "us_probe_read", "us_probe_read_sink_words",
            "us_probe_copy", "us_probe_spin")
 
@@ -82,6 +82,8 @@ def lib():
         L.us_pmr.argtypes = [ctypes.POINTER(IEBME), i32, ctypes.POINTER(PMRReport)]
         L.us_spmm_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(SpmmOpts),
                                              ctypes.POINTER(sz)]
+        pi32 = ctypes.POINTER(i32)
+        L.us_spmm_plan.argtypes = [i32, i32, i32, ctypes.POINTER(SpmmOpts), pi32, pi32, pi32]
         L.us_spmm.argtypes = [ctypes.POINTER(IEBMEDev), vp, i32, vp, vp, vp, vp, sz,
                               ctypes.POINTER(SpmmOpts), vp]
         L.us_gemm_i8.argtypes = [vp, vp, i32, i32, i32, vp, vp]
@@ -92,7 +94,7 @@ def lib():
         L.us_probe_read_sink_words.restype = sz
         L.us_probe_copy.argtypes = [vp, vp, sz, vp]
         L.us_probe_spin.argtypes = [ctypes.c_uint64, vp]
-        for name in ("us_encode", "us_pmr", "us_spmm_workspace_size", "us_spmm", "us_gemm_i8",
+        for name in ("us_encode", "us_pmr", "us_spmm_workspace_size", "us_spmm_plan", "us_spmm", "us_gemm_i8",
                      "us_probe_read", "us_probe_copy", "us_probe_spin"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -226,6 +228,15 @@ def workspace_size(M: int, K: int, N: int, split_k: int = 0) -> int:
     _check("us_spmm_workspace_size",
            lib().us_spmm_workspace_size(M, K, N, ctypes.byref(opts), ctypes.byref(n)))
     return n.value
+
+
+def spmm_plan(M: int, K: int, N: int, split_k: int = 0, variant: int = 0):
+    """us_spmm_plan: (K slices per row block, LTs per chunk, staging 1 whole / 2 ring)."""
+    opts = SpmmOpts(split_k, variant)
+    a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    _check("us_spmm_plan", lib().us_spmm_plan(M, K, N, ctypes.byref(opts), ctypes.byref(a),
+                                              ctypes.byref(b), ctypes.byref(c)))
+    return a.value, b.value, c.value
 
 
 def spmm(w: DeviceEncoded, x_packed, N: int, y, scale=None, y_f32=None, split_k: int = 0,

@@ -17,8 +17,12 @@
 //    its payload with 16-byte buffer loads (a few in flight, the rest issued
 //    as earlier ones land) while the bitmaps and the activation slice, which
 //    were requested together with the offsets, are copied into the
-//    wavefront's own LDS stage. A wavefront's LDS accesses execute in order,
-//    so no workgroup barrier is needed between staging and decoding.
+//    wavefront's own LDS stage. The payload is staged whole or through a
+//    4 KB ring (see Chunk); a slice of several chunks requests the next
+//    chunk's inputs ahead of the current payload. A wavefront's LDS accesses
+//    execute in order, so no workgroup barrier is needed between staging
+//    and decoding. The host picks the split, the chunk length and the
+//    staging per shape (choose_config).
 //
 //  * Decode (the paper's LSPD, Section VI-B). One LT (16 x 64) is decoded by
 //    one wavefront straight into the A operand of v_mfma_i32_16x16x64_i8.
@@ -641,6 +645,31 @@ int device_cus() {
 }
 
 }  // namespace
+
+extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, const us_spmm_opts *opts, int32_t *split_k,
+                                  int32_t *chunk_lts, int32_t *staging) {
+    if (!split_k || !chunk_lts || !staging) return US_ERR_ARG;
+    if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
+    if (N < 1 || N > US_N_MAX) return US_ERR_SHAPE;
+    int wpg_only = 0, stg = 0;
+    if (opts) {
+        if (opts->variant < 0 || opts->variant > 2) return US_ERR_ARG;
+        stg = opts->variant;
+        const int s = opts->split_k;
+        if (s != 0) {
+            if (s != 1 && s != 2 && s != 4 && s != 8 && s != 16) return US_ERR_ARG;
+            wpg_only = s;
+            while (wpg_only > K / US_LT_W) wpg_only /= 2;
+        }
+    }
+    int wpg = 0, cfg = -1;
+    choose_config(M, K, N, device_cus(), wpg_only, stg, wpg, cfg);
+    if (cfg < 0) return US_ERR_ARG;
+    *split_k = wpg;
+    *chunk_lts = kCfgs[cfg].ch;
+    *staging = kCfgs[cfg].ring ? 2 : 1;
+    return US_OK;
+}
 
 extern "C" us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, const us_spmm_opts *opts,
                                             size_t *bytes) {

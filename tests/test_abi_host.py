@@ -232,3 +232,53 @@ def test_probe_argument_errors():
 def test_pack_int4_layout():
     Xt = np.array([[-8, 7, 0, -1]], dtype=np.int8)
     assert binding.pack_int4(Xt).tolist() == [[0x78, 0xF0]]
+
+
+# The launch plan (host only; with no GPU visible the library plans for a
+# 256-CU MI355X, which is also what the GPU reports).
+@pytest.mark.parametrize("M,K,N,plan", [
+    (4096, 11008, 8, (16, 11, 1)),     # one generation of 16-wavefront workgroups
+    (12288, 4096, 8, (4, 16, 2)),      # the ring lets three workgroups share a CU
+    (28672, 8192, 1, (2, 16, 1)),      # four chunks per slice, one generation
+    (28672, 8192, 32, (2, 4, 1)),      # two column blocks: at most 4 slices
+])
+def test_plan_choices(M, K, N, plan):
+    assert binding.spmm_plan(M, K, N) == plan
+
+
+@pytest.mark.parametrize("M,K", [(16, 64), (512, 512), (4096, 11008), (12288, 4096), (48, 130048)])
+@pytest.mark.parametrize("N", [1, 8, 16, 17, 32])
+def test_plan_invariants(M, K, N):
+    nkb = K // 64
+    for split in (0, 1, 2, 4, 8, 16):
+        for variant in (0, 1, 2):
+            if variant == 2 and N > 16:
+                with pytest.raises(binding.UsError):
+                    binding.spmm_plan(M, K, N, split, variant)
+                continue
+            try:
+                s, ch, stg = binding.spmm_plan(M, K, N, split, variant)
+            except binding.UsError:
+                # A forced ring with a fixed split may fit no configuration;
+                # automatic choices always fit.
+                assert variant == 2 and split != 0
+                continue
+            assert s in (1, 2, 4, 8, 16) and s <= nkb
+            if split:
+                assert s == min(split, 1 << (nkb.bit_length() - 1))
+            assert ch in ((4, 8) if N > 16 else (4, 8, 11, 16))
+            assert stg in (1, 2) and (variant == 0 or stg == variant)
+            assert stg == 1 or ch == 16
+
+
+def test_plan_argument_errors():
+    L = binding.lib()
+    a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    ok = ctypes.byref(binding.SpmmOpts(0, 0))
+    assert L.us_spmm_plan(32, 128, 8, ok, None, ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(40, 128, 8, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
+    assert L.us_spmm_plan(32, 128, 33, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
+    bad = ctypes.byref(binding.SpmmOpts(3, 0))
+    assert L.us_spmm_plan(32, 128, 8, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
+    bad = ctypes.byref(binding.SpmmOpts(0, 5))
+    assert L.us_spmm_plan(32, 128, 8, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
