@@ -124,6 +124,34 @@ def test_ring_refused_for_two_column_blocks(torch_cuda):
         run_spmm(torch_cuda, W, Xt, variant=2)
 
 
+def _random_cases(n, seed=20261202):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for k in range(n):
+        M = 16 * int(rng.integers(1, 9))
+        K = 64 * int(rng.integers(1, 90))
+        N = int(rng.integers(1, 33))
+        s = float(rng.choice([0.0, 0.3, 0.5, 0.7, 0.9, 1.0]))
+        split = int(rng.choice([0, 0, 1, 2, 4, 8, 16]))
+        variant = 0 if N > 16 else int(rng.choice([0, 1, 2]))
+        cases.append((M, K, N, s, split, variant, 500 + k))
+    return cases
+
+
+@pytest.mark.parametrize("M,K,N,s,split_k,variant,seed", _random_cases(40))
+def test_random_shapes(torch_cuda, M, K, N, s, split_k, variant, seed):
+    """Seeded random shapes, widths, densities, splits and stagings."""
+    announce(f"random M={M} K={K} N={N} s={s} split={split_k} variant={variant} seed={seed}")
+    W, Xt, sc = synth.random_problem(M, K, N, s, seed)
+    try:
+        Y, Yf = run_spmm(torch_cuda, W, Xt, sc, split_k=split_k, variant=variant)
+    except binding.UsError:
+        # only a forced ring with a fixed split may fit no configuration
+        assert variant == 2 and split_k != 0
+        return
+    check(Y, Yf, W, Xt, sc)
+
+
 def test_row_skewed_density(torch_cuda):
     announce("row skew M=256 K=2048 N=16")
     W, Xt, _ = synth.random_problem(256, 2048, 16, 0.6, 21, row_skew=True)
