@@ -55,7 +55,7 @@
 #include "us.h"
 
 #ifndef US_SPMM_WINDOW
-#define US_SPMM_WINDOW 3
+#define US_SPMM_WINDOW 2
 #endif
 
 namespace {
