@@ -1,11 +1,13 @@
 #!/usr/bin/env python3
 """Benchmark of the W4A4 IE-BME SpMM on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--N n] [--split-k S]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--N n] [--split-k S] [--reorder]
 
 One step is one us_spmm call (stream the IE-BME tiles, decode, multiply,
 combine, store Y and the dequantised Y) over one copy of the encoded weight
 matrix; the encoding itself is offline, as in the paper, and is not timed.
+With --reorder the matrix is encoded after bitmap-aware row reordering
+(Section V-B) and the kernel undoes the row permutation of every tile.
 Every timed batch queues its launches behind a bounded spin kernel, so the
 GPU runs them back to back and host launch cost never enters the event
 timings; the weight copies rotate over at least 1 GiB so that none of them
@@ -34,29 +36,36 @@ DEFAULT_WORKLOAD = "ffn_down_4096x11008_s50"
 HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 1 << 30
 ROUND_LAUNCHES = 200
-KERNEL_SRC = os.path.join(ROOT, "paper_2608_09291_amd", "csrc", "us_spmm.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_09291_amd", "csrc", f)
+               for f in ("us_spmm_kernel.h", "us_spmm.hip", "us_spmm_perm.hip")]
 
 # HBM traffic of one SpMM launch, read from rocprofv3 --pmc runs of this
 # script (one pass for FETCH_SIZE, one for WRITE_SIZE; KiB per dispatch), each
 # divided by what the same counter reads per byte for the plain copy kernel
 # (bench.py --copy-probe 268435456: FETCH_SIZE reads 0.5 KiB and WRITE_SIZE
-# 1.0 KiB per KiB copied). An entry holds only for the kernel source whose
-# SHA-256 starts with `src`; after any change to it the traffic is unknown.
+# 1.0 KiB per KiB copied). An entry holds only for the kernel sources whose
+# SHA-256 (of the files in KERNEL_SRCS, concatenated) starts with `src`;
+# after any change to them the traffic is unknown. Keyed by workload, N and
+# row reordering.
 COPY_FACTOR = {"FETCH_SIZE": 0.5, "WRITE_SIZE": 1.0}
 MEASURED_TRAFFIC = {
-    ("ffn_down_4096x11008_s50", 8): dict(src="f2cdb058f8e4b438", FETCH_SIZE=11374.8, WRITE_SIZE=256.0),
 }
 
 
-def measured_traffic(workload: str, N: int):
-    """Counter-derived HBM bytes per launch, or None if not measured for this kernel source."""
+def kernel_source_hash() -> str:
     import hashlib
-    e = MEASURED_TRAFFIC.get((workload, N))
-    if e is None:
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, N: int, reordered: bool):
+    """Counter-derived HBM bytes per launch, or None if not measured for this kernel source."""
+    e = MEASURED_TRAFFIC.get((workload, N, reordered))
+    if e is None or not kernel_source_hash().startswith(e["src"]):
         return None
-    with open(KERNEL_SRC, "rb") as f:
-        if not hashlib.sha256(f.read()).hexdigest().startswith(e["src"]):
-            return None
     return int(round(sum(e[c] / COPY_FACTOR[c] for c in COPY_FACTOR) * 1024))
 
 
@@ -72,6 +81,7 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(synth.WORKLOADS))
     ap.add_argument("--N", type=int, default=0, help="activation columns (default: the workload's first)")
     ap.add_argument("--split-k", type=int, default=0)
+    ap.add_argument("--reorder", action="store_true", help="row-reorder the LTs before encoding")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extras", action="store_true", help="skip the read-ceiling and dense GEMM points")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -120,17 +130,19 @@ class Timer:
         return total
 
 
-def spmm_bench(torch, args, w, N, timer):
+def spmm_bench(torch, args, w, N, timer, reorder=False):
     W = synth.weights(w)
     Xt = synth.activations(w, N)
-    enc = binding.encode(W)
+    enc = binding.encode(W, reorder=reorder)
     rep = binding.pmr(enc, N)
     dev0 = binding.to_device(enc)
     enc_bytes = dev0.nbytes
     n_copies = max(2, -(-ROTATE_BYTES // enc_bytes))
     copies = [dev0] + [binding.DeviceEncoded(dev0.bitmaps.clone(), dev0.offsets.clone(),
                                              dev0.payload.clone(), dev0.M, dev0.K, dev0.n_lt,
-                                             dev0.n_payload) for _ in range(n_copies - 1)]
+                                             dev0.n_payload,
+                                             None if dev0.perm is None else dev0.perm.clone())
+                       for _ in range(n_copies - 1)]
     xp = torch.from_numpy(binding.pack_int4(Xt)).cuda()
     y = torch.empty((N, w.M), dtype=torch.int32, device="cuda")
     sc = yf = None
@@ -162,9 +174,10 @@ def spmm_bench(torch, args, w, N, timer):
         raise binding.UsError("us_spmm", status[0])
 
     # Algorithmic bytes of one call: stored payload (zeros of active groups
-    # included), bitmaps (32 B/LT), offsets (4 B/LT), X, Y, and with the
-    # dequant epilogue the scales and the float32 Y.
-    alg = (rep["payload_stored_bytes"] + rep["bitmap_bytes"] + rep["offset_bytes"]
+    # included), bitmaps (32 B/LT), offsets (4 B/LT), row permutations (8 B/LT
+    # when reordered), X, Y, and with the dequant epilogue the scales and the
+    # float32 Y.
+    alg = (rep["payload_stored_bytes"] + rep["bitmap_bytes"] + rep["offset_bytes"] + rep["perm_bytes"]
            + w.K * N // 2 + w.M * N * 4)
     if w.dequant:
         alg += w.M * 4 + w.M * N * 4
@@ -256,7 +269,7 @@ def main():
     timer = Timer(torch)
 
     log(f"[bench] workload {w.name} M={w.M} K={w.K} N={N} s={w.sparsity} dequant={w.dequant}")
-    r = spmm_bench(torch, args, w, N, timer)
+    r = spmm_bench(torch, args, w, N, timer, reorder=args.reorder)
     ms_step = r["ms"] / args.steps
     us = ms_step * 1e3
     gbs = r["alg_bytes"] / (ms_step * 1e-3) / 1e9
@@ -282,7 +295,7 @@ def main():
         log(f"[bench] cpu oracle {cpu['ms_per_call']} ms/call on {cpu['cores']} threads")
 
     rep = r["rep"]
-    plan = binding.spmm_plan(w.M, w.K, N, args.split_k)
+    plan = binding.spmm_plan(w.M, w.K, N, args.split_k, reordered=args.reorder)
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -297,7 +310,7 @@ def main():
         "dtype": "int8",
         "data": "synthetic",
         "config": {"workload": w.name, "M": w.M, "K": w.K, "N": N, "sparsity": w.sparsity,
-                   "dequant": w.dequant, "split_k": plan[0], "chunk_lts": plan[1],
+                   "dequant": w.dequant, "reordered": args.reorder, "split_k": plan[0], "chunk_lts": plan[1],
                    "staging": "ring" if plan[2] == 2 else "whole", "plan": "auto" if not args.split_k else "forced",
                    "weights": "w4a4 IE-BME (16x64 tiles, 2x2 areas), int8 MFMA, int32 accumulate",
                    "rotating_copies": r["n_copies"]},
@@ -309,7 +322,7 @@ def main():
         "ci_eff_eq2": round(rep["ci_eff"], 3),
         "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(w.name, N),
+                     "traffic": measured_traffic(w.name, N, args.reorder),
                      "kernel": "us_spmm_kernel",
                      "bytes_per_launch": r["alg_bytes"]},
         "cpu_baseline": cpu,

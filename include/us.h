@@ -60,7 +60,14 @@ typedef enum {
  * row-major) is area q's value at (i, j); value n is the low nibble of byte
  * n / 2 when n is even, the high nibble when odd, in two's complement.
  *
- * The three arrays are allocated by us_encode and freed by us_iebme_free.
+ * Row reordering (Section V-B) is recorded in `perm`. When it is NULL the
+ * LTs keep their row order. Otherwise bits 4p .. 4p + 3 of perm[t] hold
+ * pi_t[p], the row of LT t that was moved to row p before encoding. The
+ * bitmaps, offsets and payload then describe the reordered LTs: rows
+ * pi_t[i] and pi_t[8 + i] of the original LT share union-mask row i.
+ *
+ * The arrays are allocated by us_encode / us_encode_reordered and freed by
+ * us_iebme_free.
  */
 typedef struct {
     int32_t M, K;                 /* weight matrix is M x K                 */
@@ -72,6 +79,7 @@ typedef struct {
     uint64_t *bitmaps;            /* n_lt * 4 words                         */
     uint32_t *offsets;            /* n_lt + 1 entries                       */
     uint8_t *payload;             /* payload_bytes bytes, zeroed padding    */
+    uint64_t *perm;               /* NULL, or n_lt row permutations         */
 } us_iebme;
 
 /*
@@ -84,6 +92,20 @@ typedef struct {
  * Returns US_ERR_ARG, US_ERR_SHAPE, US_ERR_RANGE or US_ERR_NOMEM on failure.
  */
 us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out);
+
+/*
+ * us_encode_reordered - bitmap-aware row reordering followed by IE-BME
+ * (Section V-B, then Section V-A). Each LT's 16 rows are split into 8 pairs
+ * that activate the fewest union-mask entries in total (Eq. 3-5, solved
+ * exactly by the grouped subset DP). The result is deterministic:
+ *   - ties keep the first optimal partner, in increasing row order, of the
+ *     smallest remaining row;
+ *   - the pairs are sorted, and pi_t lists the first rows of all pairs,
+ *     then the second rows (the canonical permutation of Section V-B).
+ * Same arguments and errors as us_encode; `out->perm` is allocated. Offline
+ * work: about 20 us of one CPU thread per LT, spread over all threads.
+ */
+us_status us_encode_reordered(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out);
 
 /* us_iebme_free - release the arrays of an encoded matrix and zero it. */
 void us_iebme_free(us_iebme *m);
@@ -105,6 +127,8 @@ typedef struct {
     double pmr;                   /* Eq. 1: payload_useful_bytes / meta_bytes  */
     double pmr_stored;            /* stored payload bytes / meta_bytes         */
     double ci_eff;                /* Eq. 2 for activation width N, as printed  */
+    int64_t perm_bytes;           /* 8 n_lt with row reordering, else 0; not
+                                     part of Stor_meta (Eq. 1 predates it)     */
 } us_pmr_report;
 
 /*
@@ -120,6 +144,9 @@ typedef struct {
     const uint8_t *payload;       /* device, ceil(n_payload / 2) + US_PAYLOAD_PAD bytes */
     int32_t M, K;
     int64_t n_lt, n_payload;
+    const uint64_t *perm;         /* device, n_lt words, 8-byte aligned, or NULL
+                                     (see us_iebme); words that are not
+                                     permutations give unspecified Y       */
 } us_iebme_dev;
 
 typedef struct {
@@ -135,12 +162,13 @@ typedef struct {
  * us_spmm_plan - the launch configuration us_spmm would use for this shape
  * and options on the current device (a 256-CU MI355X when no device is
  * visible): K slices per 16-row block (one wavefront each), LTs per chunk,
- * and payload staging (1 whole chunk, 2 ring). Host only; for tuning and
- * reporting. Same argument errors as us_spmm; US_ERR_ARG if no
- * configuration fits.
+ * and payload staging (1 whole chunk, 2 ring). `reordered` != 0 plans for a
+ * matrix with row permutations (us_iebme_dev.perm != NULL), whose stages
+ * are larger. Host only; for tuning and reporting. Same argument errors as
+ * us_spmm; US_ERR_ARG if no configuration fits.
  */
-us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, const us_spmm_opts *opts, int32_t *split_k,
-                       int32_t *chunk_lts, int32_t *staging);
+us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t reordered, const us_spmm_opts *opts,
+                       int32_t *split_k, int32_t *chunk_lts, int32_t *staging);
 
 /*
  * us_spmm_workspace_size - device workspace bytes us_spmm needs for this
@@ -153,7 +181,8 @@ us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, const us_spmm_
  * us_spmm - Y = W X on the GPU: W in IE-BME (device copy), X dense INT4,
  * INT32 accumulation (Section VI, "UnionSparse Kernel" algorithm: the kernel
  * takes the IE-BME matrix, the activations and a split-K count, and returns Y).
- *   w      : encoded matrix, device arrays
+ *   w      : encoded matrix, device arrays; with w->perm the LTs are
+ *            row-reordered (Section V-B) and Y is still in original row order
  *   x      : device, N x K row-major INT4, two values per byte along K
  *            (even k in the low nibble), 16-byte aligned
  *   N      : 1..32 activation columns

@@ -1,8 +1,10 @@
-// Host side of the IE-BME format: encoder (Section V-A) and byte accounting
-// (Eq. 1, Eq. 2). Runs offline on the CPU, as the paper's format conversion
-// does; its cost is not part of the SpMM latency.
+// Host side of the IE-BME format: encoder (Section V-A), bitmap-aware row
+// reordering (Section V-B) and byte accounting (Eq. 1, Eq. 2). Runs offline
+// on the CPU, as the paper's format conversion does; its cost is not part of
+// the SpMM latency.
 #include <algorithm>
 #include <atomic>
+#include <climits>
 #include <cstdlib>
 #include <cstring>
 #include <thread>
@@ -33,13 +35,80 @@ void parallel_ranges(int64_t n, F body) {
 
 inline int popcount64(uint64_t v) { return __builtin_popcountll(v); }
 
-// Value of area q at union-mask position (i, j) of the LT whose top-left
-// element is `base`: area q = a * C_A + c covers LT rows [8a, 8a+8) and
-// columns [32c, 32c+32).
-inline int8_t area_value(const int8_t *base, int64_t ldw, int q, int i, int j) {
+// Value of area q at union-mask position (i, j) of an LT whose (possibly
+// reordered) rows are `rows`: area q = a * C_A + c covers rows [8a, 8a+8)
+// and columns [32c, 32c+32).
+inline int8_t area_value(const int8_t *const *rows, int q, int i, int j) {
     const int a = q / US_CA, c = q % US_CA;
-    return base[(int64_t)(a * kAreaH + i) * ldw + c * kAreaW + j];
+    return rows[a * kAreaH + i][c * kAreaW + j];
 }
+
+// Bitmap-aware row reordering of one LT (Section V-B) for R_A = C_A = 2.
+//
+// With two area columns, row r activates grouped column j (Eq. 3) when it is
+// nonzero at column j or j + 32: `fold[r]` holds those 32 bits. A pair of
+// rows then costs popcount(fold[r] | fold[s]) union-mask entries (Eq. 4),
+// and Eq. 5 pairs up all 16 rows at minimum total cost. The DP state is the
+// set of rows still unpaired; each step pairs its lowest row with one other
+// row, so only row sets reachable that way are visited (1596 of 2^16).
+class RowPairing {
+public:
+    // Canonical permutation: pi[g] and pi[8 + g] are the rows of pair g,
+    // pairs sorted by their first row. Returns the minimum cost.
+    int solve(const uint32_t fold[US_LT_H], uint8_t pi[US_LT_H]) {
+        for (int r = 0; r < US_LT_H; ++r)
+            for (int s = 0; s < US_LT_H; ++s) cost_[r][s] = (uint8_t)__builtin_popcount(fold[r] | fold[s]);
+        if (++gen_ == 0) {                       // stamps wrapped: forget everything
+            std::fill(stamp_.begin(), stamp_.end(), 0u);
+            gen_ = 1;
+        }
+        const uint32_t all = (1u << US_LT_H) - 1u;
+        const int total = best(all);
+        // The lowest unpaired row grows from step to step, so the pairs come
+        // out sorted and each pair's first row is its smaller one.
+        uint32_t left = all;
+        for (int g = 0; g < US_LT_H / 2; ++g) {
+            const int r = __builtin_ctz(left);
+            const int s = partner_[left];
+            pi[g] = (uint8_t)r;
+            pi[US_LT_H / 2 + g] = (uint8_t)s;
+            left &= ~((1u << r) | (1u << s));
+        }
+        return total;
+    }
+
+private:
+    // F(left): minimum cost of pairing the rows in `left`. Partners are
+    // tried in increasing row order and only a strictly lower cost replaces
+    // the current choice.
+    int best(uint32_t left) {
+        if (left == 0) return 0;
+        if (stamp_[left] == gen_) return value_[left];
+        const int r = __builtin_ctz(left);
+        const uint32_t others = left & (left - 1u);
+        int min_cost = INT_MAX, arg = -1;
+        for (uint32_t x = others; x; x &= x - 1u) {
+            const int s = __builtin_ctz(x);
+            const int v = cost_[r][s] + best(others & ~(1u << s));
+            if (v < min_cost) {
+                min_cost = v;
+                arg = s;
+            }
+        }
+        stamp_[left] = gen_;
+        value_[left] = (uint16_t)min_cost;
+        partner_[left] = (uint8_t)arg;
+        return min_cost;
+    }
+
+    uint8_t cost_[US_LT_H][US_LT_H];
+    std::vector<uint32_t> stamp_ = std::vector<uint32_t>(1u << US_LT_H, 0u);
+    std::vector<uint16_t> value_ = std::vector<uint16_t>(1u << US_LT_H);
+    std::vector<uint8_t> partner_ = std::vector<uint8_t>(1u << US_LT_H);
+    uint32_t gen_ = 0;
+};
+
+us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool reorder, us_iebme *out);
 
 }  // namespace
 
@@ -57,6 +126,16 @@ extern "C" const char *us_status_string(us_status s) {
 }
 
 extern "C" us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out) {
+    return encode_impl(w, M, K, ldw, false, out);
+}
+
+extern "C" us_status us_encode_reordered(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out) {
+    return encode_impl(w, M, K, ldw, true, out);
+}
+
+namespace {
+
+us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool reorder, us_iebme *out) {
     if (!w || !out) return US_ERR_ARG;
     if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W) return US_ERR_SHAPE;
     if (ldw < K) return US_ERR_ARG;
@@ -77,34 +156,73 @@ extern "C" us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ld
     const int64_t n_lt = (int64_t)(M / US_LT_H) * nkb;
     uint64_t *bitmaps = (uint64_t *)std::calloc((size_t)n_lt * US_WORDS_PER_LT, sizeof(uint64_t));
     uint32_t *offsets = (uint32_t *)std::calloc((size_t)n_lt + 1, sizeof(uint32_t));
+    uint64_t *perm = reorder ? (uint64_t *)std::calloc((size_t)n_lt, sizeof(uint64_t)) : nullptr;
     std::vector<uint32_t> P;
-    std::vector<int64_t> nnz_part;
     try {
         P.resize((size_t)n_lt);
     } catch (...) {
         std::free(bitmaps);
         std::free(offsets);
+        std::free(perm);
         return US_ERR_NOMEM;
     }
-    if (!bitmaps || !offsets) {
+    if (!bitmaps || !offsets || (reorder && !perm)) {
         std::free(bitmaps);
         std::free(offsets);
+        std::free(perm);
         return US_ERR_NOMEM;
     }
 
-    // Pass 1: shared union mask B_t and P_t = ||B_t||_0 per LT; count nonzeros.
+    // Rows of LT t in encoding order: the identity, or pi_t from perm[t].
+    auto lt_rows = [&](int64_t t, const int8_t *rows[US_LT_H]) {
+        const int8_t *base = w + (t / nkb) * US_LT_H * ldw + (t % nkb) * US_LT_W;
+        for (int p = 0; p < US_LT_H; ++p) {
+            const int r = perm ? (int)((perm[t] >> (4 * p)) & 0xF) : p;
+            rows[p] = base + (int64_t)r * ldw;
+        }
+    };
+
+    // Pass 1: row reordering (optional), then the shared union mask B_t and
+    // P_t = ||B_t||_0 per LT; count nonzeros.
     std::atomic<int64_t> nnz{0};
+    std::atomic<bool> oom{false};
     parallel_ranges(n_lt, [&](int64_t t0, int64_t t1) {
+        RowPairing *dp = nullptr;
+        if (reorder) {
+            try {
+                dp = new RowPairing();
+            } catch (...) {
+                oom = true;
+                return;
+            }
+        }
         int64_t local_nnz = 0;
         for (int64_t t = t0; t < t1; ++t) {
-            const int8_t *base = w + (t / nkb) * US_LT_H * ldw + (t % nkb) * US_LT_W;
+            if (dp) {
+                const int8_t *base = w + (t / nkb) * US_LT_H * ldw + (t % nkb) * US_LT_W;
+                uint32_t fold[US_LT_H];
+                for (int r = 0; r < US_LT_H; ++r) {
+                    const int8_t *row = base + (int64_t)r * ldw;
+                    uint32_t f = 0;
+                    for (int j = 0; j < kAreaW; ++j)
+                        if (row[j] != 0 || row[kAreaW + j] != 0) f |= 1u << j;
+                    fold[r] = f;
+                }
+                uint8_t pi[US_LT_H];
+                dp->solve(fold, pi);
+                uint64_t word = 0;
+                for (int p = 0; p < US_LT_H; ++p) word |= (uint64_t)pi[p] << (4 * p);
+                perm[t] = word;
+            }
+            const int8_t *rows[US_LT_H];
+            lt_rows(t, rows);
             uint64_t *bm = bitmaps + t * US_WORDS_PER_LT;
             uint32_t p = 0;
             for (int i = 0; i < kAreaH; ++i) {
                 for (int j = 0; j < kAreaW; ++j) {
                     bool any = false;
                     for (int q = 0; q < US_RA * US_CA; ++q) {
-                        const bool nz = area_value(base, ldw, q, i, j) != 0;
+                        const bool nz = area_value(rows, q, i, j) != 0;
                         local_nnz += nz;
                         any |= nz;
                     }
@@ -117,8 +235,15 @@ extern "C" us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ld
             }
             P[(size_t)t] = p;
         }
+        delete dp;
         nnz += local_nnz;
     });
+    if (oom) {
+        std::free(bitmaps);
+        std::free(offsets);
+        std::free(perm);
+        return US_ERR_NOMEM;
+    }
 
     // Union Value Offsets: o_t = sum over earlier LTs of Q * P_tau.
     uint64_t run = 0;
@@ -133,6 +258,7 @@ extern "C" us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ld
     if (!payload) {
         std::free(bitmaps);
         std::free(offsets);
+        std::free(perm);
         return US_ERR_NOMEM;
     }
 
@@ -141,7 +267,8 @@ extern "C" us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ld
     // a multiple of four values, so LTs never share a byte.
     parallel_ranges(n_lt, [&](int64_t t0, int64_t t1) {
         for (int64_t t = t0; t < t1; ++t) {
-            const int8_t *base = w + (t / nkb) * US_LT_H * ldw + (t % nkb) * US_LT_W;
+            const int8_t *rows[US_LT_H];
+            lt_rows(t, rows);
             const uint64_t *bm = bitmaps + t * US_WORDS_PER_LT;
             const uint64_t o = offsets[t];
             const uint64_t Pt = P[(size_t)t];
@@ -151,7 +278,7 @@ extern "C" us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ld
                 const int i = L / kAreaW, j = L % kAreaW;
                 for (int q = 0; q < US_RA * US_CA; ++q) {
                     const uint64_t n = o + (uint64_t)q * Pt + rho;
-                    const uint8_t nib = (uint8_t)area_value(base, ldw, q, i, j) & 0xF;
+                    const uint8_t nib = (uint8_t)area_value(rows, q, i, j) & 0xF;
                     payload[n >> 1] |= (uint8_t)(nib << ((n & 1) * 4));
                 }
                 ++rho;
@@ -172,14 +299,18 @@ extern "C" us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ld
     out->bitmaps = bitmaps;
     out->offsets = offsets;
     out->payload = payload;
+    out->perm = perm;
     return US_OK;
 }
+
+}  // namespace
 
 extern "C" void us_iebme_free(us_iebme *m) {
     if (!m) return;
     std::free(m->bitmaps);
     std::free(m->offsets);
     std::free(m->payload);
+    std::free(m->perm);
     std::memset(m, 0, sizeof(*m));
 }
 
@@ -216,6 +347,7 @@ extern "C" us_status us_pmr(const us_iebme *m, int32_t N, us_pmr_report *out) {
     r.payload_useful_bytes = bw * (double)m->nnz;
     r.pmr = r.payload_useful_bytes / (double)r.meta_bytes;
     r.pmr_stored = bw * (double)m->n_payload / (double)r.meta_bytes;
+    r.perm_bytes = m->perm ? 8 * n_lt : 0;
     if (N > 0 && m->nnz > 0) {
         // Eq. 2 as printed: 2 M N (1-s) / (B_w M (1-s)(1 + 1/PMR) + B_w N).
         const double keep = (double)m->nnz / ((double)m->M * (double)m->K);

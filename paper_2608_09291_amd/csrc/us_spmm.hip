@@ -1,585 +1,17 @@
-// IE-BME x INT4 -> INT32 sparse product on gfx950 (CDNA4).
-//
-// The operation is the UnionSparse kernel of Section VI: Y = W X with W in
-// IE-BME (Section V-A), X dense INT4, INT32 accumulation. What is kept from
-// the paper and what is re-designed for CDNA4:
-//
-//  * Work split. One workgroup per 16-row block of W; its wavefronts split the
-//    block's K range into contiguous slices (the paper's split-K with its
-//    InitSchedule and Reduction steps). Because every slice of a row block
-//    lives in one workgroup, the split-K sums are combined in LDS at the end:
-//    no workspace, no second launch. In row-block-major LT order a slice is a
-//    contiguous run of LTs, so its bitmaps and payload are contiguous bytes.
-//
-//  * Staging (the paper's producer/consumer pipeline, re-cut for CDNA4). A
-//    wavefront's slice is processed in chunks of up to CH LTs, normally one.
-//    For a chunk the wavefront first reads the chunk's offsets, then streams
-//    its payload with 16-byte buffer loads (a few in flight, the rest issued
-//    as earlier ones land) while the bitmaps and the activation slice, which
-//    were requested together with the offsets, are copied into the
-//    wavefront's own LDS stage. The payload is staged whole or through a
-//    4 KB ring (see Chunk); a slice of several chunks requests the next
-//    chunk's inputs ahead of the current payload. A wavefront's LDS accesses
-//    execute in order, so no workgroup barrier is needed between staging
-//    and decoding. The host picks the split, the chunk length and the
-//    staging per shape (choose_config).
-//
-//  * Decode (the paper's LSPD, Section VI-B). One LT (16 x 64) is decoded by
-//    one wavefront straight into the A operand of v_mfma_i32_16x16x64_i8.
-//    Lane l owns MFMA row l % 16 = 2 i + a (union-mask row i, area row a) and
-//    k-group g = l / 16, which is the G = 8 bit segment g of mask row i.
-//    idx_base is split in two: the popcount of the rows before row i (plus
-//    2 P_t for area row a = 1, whose streams start two streams later) is the
-//    same for all four segments of a row, so it is computed once per LT and
-//    chunk by a DPP scan over 16 lanes and kept in LDS as a stage bit address;
-//    each lane adds the popcount of its row below bit 8 g. The same index then
-//    reads area stream q = 2a (columns 8g..8g+7) and stream q = 2a + 1
-//    (columns 32+8g..32+8g+7), the paper's "one rank reused across all area
-//    streams". Active nibbles are placed into their byte slots with two
-//    v_perm_b32 per 8 positions, selectors taken from a 256-entry table
-//    indexed by the 8-bit segment; inactive slots get selector 0x0C (zero).
-//    LTs are decoded in pairs so that two independent chains interleave.
-//
-//  * INT4 -> INT8. CDNA4 has no INT4 matrix instruction. Weights and
-//    activations are expanded to bytes that hold the value in the high
-//    nibble (16 v, exact in int8), so the MFMA sums are 256 Y; the epilogue
-//    shifts right by 8. |256 Y| <= 256 * 64 * K < 2^31 for K <= US_K_MAX.
-//    Both operands put the even and the odd positions of each 8-group in
-//    separate dwords, the same slot order on both sides of the product.
+// Host side of the IE-BME SpMM (Section VI, "UnionSparse Kernel"
+// algorithm): argument checks, the choice of split and chunk configuration,
+// and the launch. The kernel is in us_spmm_kernel.h.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include <atomic>
-#include <type_traits>
 
 #include "us.h"
-
-#ifndef US_SPMM_WINDOW
-#define US_SPMM_WINDOW 2
-#endif
+#include "us_spmm_kernel.h"
 
 namespace {
 
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) uint32_t lds_u32;
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef __attribute__((address_space(3))) u32x2 lds_u2;
-typedef __attribute__((address_space(3))) u32x4 lds_u4;
-
-constexpr uint32_t kHiNib = 0xF0F0F0F0u;
-constexpr int kWindow = US_SPMM_WINDOW;                // payload loads in flight per wavefront
-constexpr int kNonTemporal = 2;                        // buffer cache policy: nt
-constexpr int kBufferDword3 = 0x00020000;              // raw buffer, 32-bit data (gfx9 family)
-constexpr int kLutBytes = 2048;                        // 256 selector pairs (static LDS)
-constexpr int kMaxLds = 160 * 1024;
-
-// Selector pair for one 8-bit union-mask segment m. Slot s of the output
-// (dword 0: s = 0..3, dword 1: s = 4..7) holds segment position 2s (s < 4) or
-// 2(s-4)+1 (s >= 4). An active position of rank r takes the r-th packed
-// value: even r sits in byte r/2 of the "low" source, odd r in byte r/2 of the
-// "high" source (bytes 4..7 of v_perm_b32's 8-byte input).
-__device__ u32x2 perm_selectors(uint32_t m) {
-    uint32_t sel[2] = {0u, 0u};
-#pragma unroll
-    for (int s = 0; s < 8; ++s) {
-        const int pos = s < 4 ? 2 * s : 2 * (s - 4) + 1;
-        uint32_t b = 0x0Cu;                                   // v_perm: constant zero
-        if ((m >> pos) & 1u) {
-            const uint32_t r = __popc(m & ((1u << pos) - 1u));
-            b = (r & 1u) ? 4u + (r >> 1) : (r >> 1);
-        }
-        sel[s >> 2] |= b << (8 * (s & 3));
-    }
-    return (u32x2){sel[0], sel[1]};
-}
-
-// LDS stage of one chunk of CH LTs (per wavefront), in bytes from the stage start:
-//   payload : the chunk's compressed values, streamed from the 16-byte
-//             boundary at or below the chunk's first byte (up to 15 bytes
-//             early); a segment window may read 8 bytes past the last value,
-//             so a chunk needs at most 32 CH + 2 pieces of 16 bytes.
-//             Linear staging (RING = false) keeps the whole chunk. RING =
-//             true keeps a ring of four 1 KB slots (stream byte b in slot
-//             (b / 1024) mod 4), so the stage does not grow with CH: an LT
-//             spans at most 528 bytes with its window overhang, so the four
-//             slots hold every LT that is ready for decoding. The 160 bytes
-//             after the ring repeat its first 160 bytes, so windows that start
-//             past the end of the ring (by at most one stream, 128 bytes,
-//             plus a window) read on into it;
-//   bitmaps : union-mask rows, 8 dwords per LT;
-//             (this and the next three arrays have room for a whole number
-//             of 4-LT passes; entries past the chunk are never decoded)
-//   bases   : per LT and lane row rr = 2i + a, the LDS bit address of the
-//             first value of row i in area stream 2a (folded into the ring
-//             with RING; 16 dwords per LT);
-//   sd      : per LT, the number of bits of one area stream (o_{t+1} - o_t);
-//   offsets : o_t of the chunk's LTs and the end offset (CH + 1 dwords);
-//   X       : the chunk's activation slice, one row of 32 bytes per LT for
-//             each activation column; rows are 16 bytes longer than the
-//             slice so that the 16 rows read by one instruction fall in
-//             different LDS banks.
-template <int CH, bool RING>
-struct Chunk {
-    static constexpr int kPayPieces = 32 * CH + 2;
-    static constexpr int kLoads = (kPayPieces + 63) / 64;     // payload loads per lane
-    static constexpr int kRing = 4096;                        // ring: four 1 KB slots
-    static constexpr int kGuard = 160;                        // copy of the ring's first bytes
-    static constexpr int kPasses = (CH + 3) / 4;              // base passes, 4 LTs each
-    static constexpr int kLtPad = 4 * kPasses;                // per-LT arrays padded to whole passes
-    static constexpr int kBmOffset = RING ? kRing + kGuard : 16 * kPayPieces;
-    static constexpr int kBaseOffset = kBmOffset + 32 * kLtPad;
-    static constexpr int kSdOffset = kBaseOffset + 64 * kLtPad;
-    static constexpr int kOffOffset = kSdOffset + 4 * kLtPad;
-    static constexpr int kXOffset = (kOffOffset + 4 * (kLtPad + 1) + 15) & ~15;
-    static constexpr int kXRowWords = 8 * CH + 4;
-    static constexpr int kXPieces = 2 * CH;                   // 16-byte pieces of one activation row
-    static_assert(2 * CH <= 64, "bitmap rows: one 16-byte load per half LT");
-    static constexpr int bytes(int N) { return kXOffset + 4 * kXRowWords * N; }
-};
-
-struct SpmmArgs {
-    const uint32_t *bm32;   // union bitmaps as dwords: LT t owns [8t, 8t + 8)
-    const uint32_t *off;    // union value offsets, n_lt + 1
-    const uint8_t *pay;     // compressed values
-    int32_t pay_bytes;      // payload bytes rounded up to 16 (inside the pad)
-    const uint8_t *x;       // activations, N rows of K/2 bytes
-    int32_t *y;
-    const float *scale;
-    float *yf;
-    int32_t M, K, N, nkb;
-};
-
-__device__ __forceinline__ uint32_t lds_load(uint32_t addr) { return *(const lds_u32 *)(size_t)addr; }
-// Two consecutive dwords at a 4-byte aligned address.
-__device__ __forceinline__ uint2 lds_load2(uint32_t addr) { return make_uint2(lds_load(addr), lds_load(addr + 4)); }
-// An 8-byte aligned pair.
-__device__ __forceinline__ uint2 lds_load_u2(uint32_t addr) {
-    const u32x2 v = *(const lds_u2 *)(size_t)addr;
-    return make_uint2(v.x, v.y);
-}
-__device__ __forceinline__ void lds_store(uint32_t addr, uint32_t v) { *(lds_u32 *)(size_t)addr = v; }
-__device__ __forceinline__ void lds_store4(uint32_t addr, u32x4 v) { *(lds_u4 *)(size_t)addr = v; }
-
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp_row(uint32_t v) {
-    // Out-of-row source lanes read zero (bound_ctrl).
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
-}
-
-// s_waitcnt vmcnt(n): at most n of this wavefront's vector-memory loads are
-// still outstanding (they complete in issue order for this counter).
-template <int n>
-__device__ __forceinline__ void wait_vm() {
-    static_assert(n >= 0 && n < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-__device__ __forceinline__ void wait_vm_all() { wait_vm<0>(); }
-
-// f(std::integral_constant<int, U>) for U = B .. E-1, as straight-line code.
-template <int B, int E, typename F>
-__device__ __forceinline__ void static_for(F &&f) {
-    if constexpr (B < E) {
-        f(std::integral_constant<int, B>{});
-        static_for<B + 1, E>(f);
-    }
-}
-
-__device__ __forceinline__ uint32_t lane_value(uint32_t v, int lane) {
-    return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
-}
-
-// 32 bits of LDS starting at LDS bit address bn (nibble index * 4).
-__device__ __forceinline__ uint32_t window(uint32_t bn) {
-    const uint2 d = lds_load2((bn >> 3) & ~3u);
-    return __builtin_amdgcn_alignbit(d.y, d.x, bn);
-}
-
-// Eight packed INT4 values -> the two slot dwords of one segment
-// (even positions, odd positions).
-__device__ __forceinline__ int2 place(uint32_t w, uint2 sel) {
-    const uint32_t hi = w & kHiNib;            // odd ranks, already in the high nibble
-    const uint32_t lo = (w << 4) & kHiNib;     // even ranks moved up
-    return make_int2((int32_t)__builtin_amdgcn_perm(hi, lo, sel.x),
-                     (int32_t)__builtin_amdgcn_perm(hi, lo, sel.y));
-}
-
-// Decode one LT into the MFMA A operand of this lane.
-//   mrow : union-mask row i of the LT
-//   base : LDS bit address of row i's first value in area stream 2a
-//   sd   : bits of one area stream (stream 2a + 1 starts sd bits later)
-//   rot  : (8 g - 3) mod 32, so that rotating mrow right by it puts the
-//          lane's segment at bits 3..10 (the selector table's byte offset)
-__device__ __forceinline__ i32x4 decode_tile(const u32x2 *lut, uint32_t mrow, uint32_t base, uint32_t sd,
-                                             uint32_t lomask, uint32_t rot) {
-    const uint32_t bn0 = base + 4u * __popc(mrow & lomask);
-    const uint32_t bn1 = bn0 + sd;
-    const u32x2 sv = *(const u32x2 *)((const char *)lut + (__builtin_amdgcn_alignbit(mrow, mrow, rot) & 0x7F8u));
-    const uint2 sel = make_uint2(sv.x, sv.y);
-    const int2 c0 = place(window(bn0), sel);
-    const int2 c1 = place(window(bn1), sel);
-    return (i32x4){c0.x, c0.y, c1.x, c1.y};
-}
-
-// Dwords g and g + 4 of an activation row's 8 dwords for one LT.
-__device__ __forceinline__ uint2 x_pair(uint32_t addr) { return make_uint2(lds_load(addr), lds_load(addr + 16)); }
-
-__device__ __forceinline__ i32x4 unpack_x(uint2 x) {
-    return (i32x4){(int32_t)((x.x << 4) & kHiNib), (int32_t)(x.x & kHiNib),
-                   (int32_t)((x.y << 4) & kHiNib), (int32_t)(x.y & kHiNib)};
-}
-
-// MULTI: some slices take several chunks (their inputs are then requested
-// one chunk ahead); otherwise every slice is a single chunk. RING: the
-// payload is staged in a 4 KB ring instead of whole (see Chunk).
-template <int WPG, int NB, int CH, bool MULTI, bool RING>
-__global__ __launch_bounds__(64 * WPG) void us_spmm_kernel(SpmmArgs p, int stage_bytes) {
-    using C = Chunk<CH, RING>;
-    extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
-    __shared__ u32x2 lut[256];                               // selector table
-    const uint32_t lds0 = (uint32_t)(size_t)(lds_u32 *)lds;  // LDS address of the dynamic block
-
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int mb = blockIdx.x;
-    const int N = p.N;
-
-    // This wavefront's K slice: LTs t0 .. t0 + nlt - 1 of row block mb
-    // (nlt >= 1 because WPG <= K / 64).
-    const int nkb = p.nkb;
-    const int kb0 = wave * nkb / WPG;
-    const int nlt = (wave + 1) * nkb / WPG - kb0;
-    const int64_t t0 = (int64_t)mb * nkb + kb0;
-
-    // Lane roles in the decode.
-    const int rr = lane & 15;
-    const int i = rr >> 1;                                 // union-mask row
-    const int g = lane >> 4;                               // segment / MFMA k-group
-    const uint32_t amask = (rr & 1) ? ~0u : 0u;            // area row partition a = 1
-    const uint32_t lomask = (1u << (8 * g)) - 1u;          // mask bits before the segment
-    const uint32_t rot = (uint32_t)(8 * g + 29) & 31u;
-
-    const uint32_t st = lds0 + (uint32_t)(wave * stage_bytes);   // stage, LDS bytes
-    const uint32_t st_bm = st + C::kBmOffset, st_base = st + C::kBaseOffset;
-    const uint32_t st_sd = st + C::kSdOffset, st_off = st + C::kOffOffset;
-    const uint32_t st_x = st + C::kXOffset;
-
-    // Activation reads in the decode: lane (column rr, k-group g) reads dwords
-    // g and g + 4 of its row's 8 dwords for the LT. Columns >= N only feed
-    // outputs that are never stored: clamp them to a staged row.
-    uint32_t xq[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) xq[nb] = st_x + 4u * (uint32_t)(min(nb * 16 + rr, N - 1) * C::kXRowWords + g);
-
-    // Activation loads: whole rows of K/2 bytes; rows >= N read zero.
-    const int xrow_bytes = p.K / 2;
-    const __amdgpu_buffer_rsrc_t xsrc =
-        __builtin_amdgcn_make_buffer_rsrc((void *)p.x, (short)0, N * xrow_bytes, kBufferDword3);
-    // Activation staging: the chunk's N x 2 CH pieces of 16 bytes, piece
-    // q = lane + 64 u is row q / (2 CH), piece q % (2 CH). Only the loads
-    // that carry pieces are issued: the texture path, not HBM, limits how
-    // fast a CU takes them in at the start of the kernel.
-    constexpr int kXLoads = (16 * NB * C::kXPieces + 63) / 64;
-    const int x_loads = (N * C::kXPieces + 63) / 64;                           // wave-uniform
-    uint32_t xv[kXLoads], xs[kXLoads];                     // global byte offset, LDS address
-#pragma unroll
-    for (int u = 0; u < kXLoads; ++u) {
-        const int q = lane + 64 * u, n = q / C::kXPieces, pj = q % C::kXPieces;
-        xv[u] = (uint32_t)(n * xrow_bytes + 16 * pj);      // rows >= N fall outside the range: zero
-        xs[u] = n < N ? st_x + 4u * (uint32_t)(n * C::kXRowWords) + 16u * (uint32_t)pj : 0u;
-    }
-
-    i32x4 acc[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[nb] = (i32x4){0, 0, 0, 0};
-
-    // A chunk's offsets, bitmaps and activations; they are requested together
-    // (none depends on another). Addresses are clamped into the matrix.
-    uint32_t offv;
-    u32x4 pbm;
-    i32x4 px[kXLoads];
-    auto request = [&](int c0) {
-        const int cnt = min(CH, nlt - c0);                 // >= 1
-        offv = p.off[t0 + c0 + min(lane, cnt)];
-        pbm = *(const u32x4 *)(p.bm32 + 8 * (t0 + c0) + 4 * min(lane, 2 * cnt - 1));
-        const uint32_t xk = (uint32_t)(32 * (kb0 + c0));
-#pragma unroll
-        for (int u = 0; u < kXLoads; ++u)
-            if (u < x_loads) px[u] = __builtin_amdgcn_raw_buffer_load_b128(xsrc, xv[u] + xk, 0, 0);
-    };
-
-    request(0);
-    // The dequant scale of the output row this thread stores in the epilogue
-    // (outputs e = threadIdx.x + 64 WPG k all have row e mod 16), requested
-    // now so that the epilogue does not wait for it.
-    float row_scale = 0.0f;
-    if (p.scale && (int)threadIdx.x < 16 * N) row_scale = p.scale[(int64_t)mb * 16 + (threadIdx.x & 15)];
-    // Selector table, computed while the first requests fly.
-    for (int e = threadIdx.x; e < 256; e += 64 * WPG) lut[e] = perm_selectors((uint32_t)e);
-    __syncthreads();
-    __builtin_amdgcn_sched_barrier(0);                     // nothing that waits on the inputs moves above
-
-    // Chunk state shared by the staging and the decoding half.
-    int cnt = 0;
-    uint32_t A0 = 0;
-    __amdgpu_buffer_rsrc_t psrc;
-    i32x4 pf[C::kLoads];
-    auto load_piece = [&](int u) {
-        pf[u] = __builtin_amdgcn_raw_buffer_load_b128(psrc, (uint32_t)(16 * lane + 1024 * u), 0, kNonTemporal);
-    };
-
-    auto stage_chunk = [&](int c0) {
-        cnt = min(CH, nlt - c0);
-        wait_vm_all();                                     // offsets, bitmaps, activations
-
-        const uint32_t ob = lane_value(offv, 0), oe = lane_value(offv, cnt);
-        A0 = (ob >> 1) & ~15u;                             // first staged payload byte
-        const uint32_t span = (((oe - 2u * A0) >> 3) << 2) + 8u;
-        const uint32_t nq = min((span + 15u) >> 4, (uint32_t)C::kPayPieces);
-        // Payload: 16-byte pieces from A0; load u brings stage bytes
-        // [1024 u, 1024 u + 1024). Pieces past the chunk read zero (range
-        // check) and cost no memory traffic. kWindow loads are in flight per
-        // wavefront, so early pieces are not queued behind the whole
-        // machine's requests and decoding starts while the rest streams.
-        // Non-temporal: the stream does not displace the activations, which
-        // every workgroup re-reads, from L2.
-        psrc = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)(p.pay + A0), (short)0, (int)min(16u * nq, (uint32_t)p.pay_bytes - A0), kBufferDword3);
-        auto issue_window = [&]() {
-            static_for<0, kWindow>([&](auto uc) {
-                if constexpr (decltype(uc)::value < C::kLoads) load_piece(decltype(uc)::value);
-            });
-        };
-        // Bitmaps (zero past the chunk), offsets and activations into the stage.
-        auto commit_inputs = [&]() {
-            if (lane < 2 * CH) lds_store4(st_bm + 16 * lane, lane < 2 * cnt ? pbm : (u32x4){0u, 0u, 0u, 0u});
-            if (lane <= CH) lds_store(st_off + 4 * lane, offv);
-#pragma unroll
-            for (int u = 0; u < kXLoads; ++u)
-                if (u < x_loads && xs[u] != 0u) lds_store4(xs[u], (u32x4)px[u]);
-        };
-        if (MULTI && nlt - c0 > CH) {
-            // A later chunk follows: once this chunk's inputs are in LDS their
-            // registers take the next chunk's inputs, requested ahead of this
-            // chunk's payload so that the payload waits below cover them.
-            commit_inputs();
-            request(c0 + CH);
-            issue_window();
-        } else {
-            issue_window();
-            commit_inputs();
-        }
-    };
-
-    auto decode_chunk = [&](int c0) {
-
-        // Row bases: lanes 16 jj + rr handle LT j = 4 pass + jj, mask row i,
-        // area row a. The scan over the 16 lanes of a DPP row starts area row
-        // a = 1 at 2 P_t (its streams follow streams 0 and 1) and adds the
-        // popcounts of the rows before i.
-        // Payload value v of the matrix is stream bit 4 v - 8 A0, at LDS bit
-        // address 8 st + (4 v - 8 A0), taken mod 32768 with the ring.
-        const uint32_t rmask = RING ? 0x7FFFu : ~0u;
-        {
-            const uint32_t jj = (uint32_t)lane >> 4;
-            const uint32_t p_bm = st_bm + 32 * jj + 4 * i, p_off = st_off + 4 * jj;
-            const uint32_t p_base = st_base + 64 * jj + 4 * rr, p_sd = st_sd + 4 * jj;
-            uint32_t mrow[C::kPasses];
-            uint2 o[C::kPasses];
-#pragma unroll
-            for (int ps = 0; ps < C::kPasses; ++ps) {
-                mrow[ps] = lds_load(p_bm + 128 * ps);
-                o[ps] = lds_load2(p_off + 16 * ps);
-            }
-#pragma unroll
-            for (int ps = 0; ps < C::kPasses; ++ps) {
-                const uint32_t inj = amask & ((o[ps].y - o[ps].x) >> 1);
-                uint32_t ex = (uint32_t)__builtin_amdgcn_update_dpp((int)inj, (int)__popc(mrow[ps]), 0x112, 0xF,
-                                                                    0xF, false);
-                ex += dpp_row<0x112>(ex);
-                ex += dpp_row<0x114>(ex);
-                ex += dpp_row<0x118>(ex);
-                lds_store(p_base + 256 * ps, 8u * st + ((4u * (o[ps].x + ex) - 8u * A0) & rmask));
-                if (rr == 0) lds_store(p_sd + 16 * ps, o[ps].y - o[ps].x);
-            }
-        }
-        // LT k can be decoded once the pieces holding its windows have landed:
-        // o_{k+1} - 2 A0 + 16 <= 2048 (u + 1), i.e. after load u = need_k.
-        const uint32_t need = (lds_load(st_off + 4 * min(lane + 1, CH)) - 2u * A0 + 15u) >> 11;
-
-        // LDS addresses of the next LT's mask row, row base, stream length and
-        // activations for this lane; they advance as LTs are decoded. The
-        // stream-length address is the same on every lane; it is kept in a
-        // vector register so that the loop needs no scalar-to-vector moves.
-        uint32_t a_bm = st_bm + 4 * i, a_base = st_base + 4 * rr, a_sd;
-        __asm__("v_mov_b32 %0, %1" : "=v"(a_sd) : "s"(st_sd));
-        uint32_t a_x[NB];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) a_x[nb] = xq[nb];
-        auto decode_one = [&]() {
-            const uint32_t mrow = lds_load(a_bm);
-            const uint32_t base = lds_load(a_base);
-            const uint32_t sd = lds_load(a_sd);
-            const i32x4 A = decode_tile(lut, mrow, base, sd, lomask, rot);
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, unpack_x(x_pair(a_x[nb])), acc[nb], 0, 0, 0);
-                a_x[nb] += 32;
-            }
-            a_bm += 32;
-            a_base += 64;
-            a_sd += 4;
-        };
-        auto decode_two = [&]() {
-            const uint32_t m0 = lds_load(a_bm), m1 = lds_load(a_bm + 32);
-            const uint32_t b0 = lds_load(a_base), b1 = lds_load(a_base + 64);
-            const uint2 sd = lds_load2(a_sd);
-            const i32x4 A0v = decode_tile(lut, m0, b0, sd.x, lomask, rot);
-            const i32x4 A1v = decode_tile(lut, m1, b1, sd.y, lomask, rot);
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0v, unpack_x(x_pair(a_x[nb])), acc[nb], 0, 0, 0);
-                acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1v, unpack_x(x_pair(a_x[nb] + 32)), acc[nb], 0, 0, 0);
-                a_x[nb] += 64;
-            }
-            a_bm += 64;
-            a_base += 128;
-            a_sd += 8;
-        };
-
-        // The payload lands in issue order: after load u, stream bytes
-        // [0, 1024 (u + 1)) have arrived (and, with the ring, bytes from
-        // 1024 (u - 3) on are still held), so LTs with need <= u can be
-        // decoded. LTs go in pairs; one that waits for its partner waits one
-        // step at most (the partner spans at most 528 more bytes). With the
-        // ring the chunk's last LT goes alone as soon as it is ready, as
-        // later steps may refill its slots.
-        int j = 0;
-        static_for<0, C::kLoads>([&](auto uc) {
-            constexpr int u = decltype(uc)::value;
-            constexpr int later = (kWindow - 1 < C::kLoads - 1 - u) ? kWindow - 1 : C::kLoads - 1 - u;
-            wait_vm<later>();                              // piece u has landed
-            if constexpr (u + kWindow < C::kLoads) load_piece(u + kWindow);
-            if constexpr (RING) {
-                lds_store4(st + 1024 * (u & 3) + 16 * lane, (u32x4)pf[u]);
-                if ((u & 3) == 0 && lane < C::kGuard / 16) lds_store4(st + C::kRing + 16 * lane, (u32x4)pf[u]);
-            } else if (u + 1 < C::kLoads || lane + 64 * u < C::kPayPieces) {
-                lds_store4(st + 1024 * u + 16 * lane, (u32x4)pf[u]);
-            }
-            __asm__ volatile("" ::: "memory");
-            if constexpr (u + 1 < C::kLoads) {
-                const int ready = __builtin_popcountll(__builtin_amdgcn_ballot_w64(lane < cnt && need <= (uint32_t)u));
-                for (; j + 1 < ready; j += 2) decode_two();
-                if (RING && j < ready && ready == cnt) {
-                    decode_one();
-                    ++j;
-                }
-            } else {
-                for (; j + 1 < cnt; j += 2) decode_two();
-                if (j < cnt) decode_one();
-            }
-        });
-        __asm__ volatile("" ::: "memory");
-    };
-    // The first chunk is straight-line code after the prologue, so every
-    // wait above counts loads exactly; later chunks only occur for long slices.
-    // Every slice holds at least one LT (the host never splits K into more
-    // slices than LTs), so the first chunk needs no branch.
-    stage_chunk(0);
-    decode_chunk(0);
-    if constexpr (MULTI) {
-        for (int c0 = CH; c0 < nlt; c0 += CH) {
-            stage_chunk(c0);
-            decode_chunk(c0);
-        }
-    }
-
-    // Split-K combine: each wavefront leaves its 16 x (16 NB) partial in its
-    // own stage, in MFMA result layout (lane l, element v: row 4 (l / 16) + v,
-    // column l % 16); after the barrier the first 16 N threads sum the WPG
-    // partials of one output each.
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) lds_store4(st + 16 * (64 * nb + lane), (u32x4)acc[nb]);
-    __syncthreads();
-
-    for (int e = threadIdx.x; e < 16 * N; e += 64 * WPG) {
-        const int r = e & 15, n = e >> 4;
-        const int R = 2 * (r & 7) + (r >> 3);                 // W row 8a + i is MFMA row 2i + a
-        const uint32_t idx = 4u * (uint32_t)(4 * (64 * (n >> 4) + 16 * (R >> 2) + (n & 15)) + (R & 3));
-        int32_t s = 0;
-#pragma unroll
-        for (int w = 0; w < WPG; ++w) s += (int32_t)lds_load(lds0 + (uint32_t)(w * stage_bytes) + idx);
-        const int32_t yv = s >> 8;                            // exact: s = 256 Y
-        const int64_t m = (int64_t)mb * 16 + r;
-        const int64_t M = p.M;
-        p.y[n * M + m] = yv;
-        if (p.scale) p.yf[n * M + m] = (float)yv * row_scale;
-    }
-}
-
-// Chunk configurations: chunk length and payload staging (see Chunk).
-// Two MFMA column blocks (N > 16) use the short linear ones only.
-struct ChunkCfg {
-    int ch;
-    bool ring;
-};
-constexpr ChunkCfg kCfgs[] = {{4, false}, {8, false}, {11, false}, {16, false}, {16, true}};
-constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
-
-bool cfg_allowed(int idx, int N) { return N <= 16 || (kCfgs[idx].ch <= 8 && !kCfgs[idx].ring); }
-
-template <int CH, bool RING>
-int stage_bytes(int N) { return (Chunk<CH, RING>::bytes(N) + 15) & ~15; }
-
-int lds_bytes(int idx, int N, int wpg) {
-    int st = 0;
-    switch (idx) {
-        case 0: st = stage_bytes<4, false>(N); break;
-        case 1: st = stage_bytes<8, false>(N); break;
-        case 2: st = stage_bytes<11, false>(N); break;
-        case 3: st = stage_bytes<16, false>(N); break;
-        default: st = stage_bytes<16, true>(N); break;
-    }
-    return kLutBytes + wpg * st;
-}
-
-template <int WPG, int NB, int CH, bool RING>
-hipError_t launch_spmm(const SpmmArgs &a, hipStream_t s) {
-    const bool multi = (a.nkb + WPG - 1) / WPG > CH;
-    auto kern = multi ? us_spmm_kernel<WPG, NB, CH, true, RING> : us_spmm_kernel<WPG, NB, CH, false, RING>;
-    // Allow more than 64 KB of dynamic LDS (set once per instantiation).
-    static const hipError_t attr =
-        (hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, true, RING>,
-                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes),
-         hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, false, RING>,
-                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes));
-    (void)attr;
-    const int st = stage_bytes<CH, RING>(a.N);
-    hipLaunchKernelGGL(kern, dim3(a.M / 16), dim3(64 * WPG), WPG * st, s, a, st);
-    return hipGetLastError();
-}
-
-template <int NB, int CH, bool RING>
-hipError_t launch_spmm_wpg(int wpg, const SpmmArgs &a, hipStream_t s) {
-    switch (wpg) {
-        case 1: return launch_spmm<1, NB, CH, RING>(a, s);
-        case 2: return launch_spmm<2, NB, CH, RING>(a, s);
-        case 4: return launch_spmm<4, NB, CH, RING>(a, s);
-        case 8: return launch_spmm<8, NB, CH, RING>(a, s);
-        default: return launch_spmm<16, NB, CH, RING>(a, s);
-    }
-}
-
-hipError_t launch_cfg(int wpg, int idx, const SpmmArgs &a, hipStream_t s) {
-    if (a.N > 16) return idx == 1 ? launch_spmm_wpg<2, 8, false>(wpg, a, s) : launch_spmm_wpg<2, 4, false>(wpg, a, s);
-    switch (idx) {
-        case 4: return launch_spmm_wpg<1, 16, true>(wpg, a, s);
-        case 3: return launch_spmm_wpg<1, 16, false>(wpg, a, s);
-        case 2: return launch_spmm_wpg<1, 11, false>(wpg, a, s);
-        case 1: return launch_spmm_wpg<1, 8, false>(wpg, a, s);
-        default: return launch_spmm_wpg<1, 4, false>(wpg, a, s);
-    }
-}
+using namespace us_spmm_detail;
 
 bool aligned(const void *ptr, uintptr_t n) { return ((uintptr_t)ptr % n) == 0; }
 
@@ -592,8 +24,9 @@ bool aligned(const void *ptr, uintptr_t n) { return ((uintptr_t)ptr % n) == 0; }
 // cold), then to more wavefronts per CU, then to linear staging and shorter
 // chunks. Residency: LDS, and at most 16 wavefronts per CU (the kernel's
 // registers). wpg_only > 0 fixes the number of wavefronts; staging 1 or 2
-// allows linear or ring payload staging only (0: either).
-void choose_config(int M, int K, int N, int n_cu, int wpg_only, int staging, int &wpg, int &cfg) {
+// allows linear or ring payload staging only (0: either). perm: the LTs are
+// row-reordered (their stages hold two more per-LT arrays).
+void choose_config(int M, int K, int N, bool perm, int n_cu, int wpg_only, int staging, int &wpg, int &cfg) {
     const int nrb = M / 16, nkb = K / 64;
     long best[5] = {0, 0, 0, 0, 0};
     wpg = 0;
@@ -607,7 +40,7 @@ void choose_config(int M, int K, int N, int n_cu, int wpg_only, int staging, int
         for (int idx = 0; idx < kNumCfgs; ++idx) {
             if (!cfg_allowed(idx, N) || (staging == 1 && kCfgs[idx].ring) || (staging == 2 && !kCfgs[idx].ring))
                 continue;
-            const int lds = lds_bytes(idx, N, w);
+            const int lds = lds_bytes(idx, N, w, perm);
             if (lds > kMaxLds) continue;
             const int c = kCfgs[idx].ch;
             const int per_cu = max(1, min(kMaxLds / lds, 16 / w));      // resident workgroups per CU
@@ -646,8 +79,8 @@ int device_cus() {
 
 }  // namespace
 
-extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, const us_spmm_opts *opts, int32_t *split_k,
-                                  int32_t *chunk_lts, int32_t *staging) {
+extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t reordered, const us_spmm_opts *opts,
+                                  int32_t *split_k, int32_t *chunk_lts, int32_t *staging) {
     if (!split_k || !chunk_lts || !staging) return US_ERR_ARG;
     if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
     if (N < 1 || N > US_N_MAX) return US_ERR_SHAPE;
@@ -663,7 +96,7 @@ extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, const us_spmm
         }
     }
     int wpg = 0, cfg = -1;
-    choose_config(M, K, N, device_cus(), wpg_only, stg, wpg, cfg);
+    choose_config(M, K, N, reordered != 0, device_cus(), wpg_only, stg, wpg, cfg);
     if (cfg < 0) return US_ERR_ARG;
     *split_k = wpg;
     *chunk_lts = kCfgs[cfg].ch;
@@ -697,8 +130,9 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     if (w->n_payload < 0 || w->n_payload > (int64_t)M * K || w->n_payload % 4) return US_ERR_FORMAT;
     if (w->n_payload > 0 && !w->payload) return US_ERR_ARG;
     if (!aligned(w->bitmaps, 8) || !aligned(w->offsets, 4) || !aligned(x, 16) || !aligned(y, 4) ||
-        (scale && (!aligned(scale, 4) || !aligned(y_f32, 4))))
+        (scale && (!aligned(scale, 4) || !aligned(y_f32, 4))) || (w->perm && !aligned(w->perm, 8)))
         return US_ERR_ARG;
+    const bool perm = w->perm != nullptr;
 
     int wpg_only = 0, staging = 0;
     if (opts) {
@@ -712,7 +146,7 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
         }
     }
     int wpg = 0, cfg = -1;
-    choose_config(M, K, N, device_cus(), wpg_only, staging, wpg, cfg);
+    choose_config(M, K, N, perm, device_cus(), wpg_only, staging, wpg, cfg);
     if (cfg < 0) return US_ERR_ARG;                        // no configuration fits LDS
 
     SpmmArgs a;
@@ -727,12 +161,13 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     a.y = y;
     a.scale = scale;
     a.yf = y_f32;
+    a.perm32 = (const uint32_t *)w->perm;
     a.M = M;
     a.K = K;
     a.N = N;
     a.nkb = (int32_t)nkb;
 
     hipStream_t s = (hipStream_t)stream;
-    const hipError_t err = launch_cfg(wpg, cfg, a, s);
+    const hipError_t err = perm ? launch_cfg_perm(wpg, cfg, a, s) : launch_cfg<false>(wpg, cfg, a, s);
     return err == hipSuccess ? US_OK : US_ERR_DEVICE;
 }

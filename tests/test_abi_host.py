@@ -163,7 +163,7 @@ def _dev_struct(M=32, K=128, n_lt=None, n_payload=0, ptr=0x1000):
     ("null_w", -1), ("null_x", -1), ("null_y", -1), ("scale_without_yf", -1),
     ("m_not_16", -2), ("k_not_64", -2), ("k_too_big", -2), ("n_zero", -2), ("n_33", -2),
     ("n_lt_wrong", -6), ("payload_odd", -6), ("payload_too_big", -6),
-    ("split_3", -1), ("variant", -1), ("misaligned_x", -1)])
+    ("split_3", -1), ("variant", -1), ("misaligned_x", -1), ("misaligned_perm", -1)])
 def test_spmm_argument_errors_before_launch(case, status):
     """Every argument error returns before touching the GPU (pointers are fake)."""
     L = binding.lib()
@@ -203,6 +203,8 @@ def test_spmm_argument_errors_before_launch(case, status):
         opts.variant = 3
     elif case == "misaligned_x":
         x = 0x2002
+    elif case == "misaligned_perm":
+        w.perm = 0x5004
     got = L.us_spmm(wp, x, N, y, sc, yf, None, 0, ctypes.byref(opts), None)
     assert got == status
 
@@ -246,18 +248,19 @@ def test_plan_choices(M, K, N, plan):
     assert binding.spmm_plan(M, K, N) == plan
 
 
+@pytest.mark.parametrize("reordered", [False, True])
 @pytest.mark.parametrize("M,K", [(16, 64), (512, 512), (4096, 11008), (12288, 4096), (48, 130048)])
 @pytest.mark.parametrize("N", [1, 8, 16, 17, 32])
-def test_plan_invariants(M, K, N):
+def test_plan_invariants(M, K, N, reordered):
     nkb = K // 64
     for split in (0, 1, 2, 4, 8, 16):
         for variant in (0, 1, 2):
             if variant == 2 and N > 16:
                 with pytest.raises(binding.UsError):
-                    binding.spmm_plan(M, K, N, split, variant)
+                    binding.spmm_plan(M, K, N, split, variant, reordered)
                 continue
             try:
-                s, ch, stg = binding.spmm_plan(M, K, N, split, variant)
+                s, ch, stg = binding.spmm_plan(M, K, N, split, variant, reordered)
             except binding.UsError:
                 # A forced ring with a fixed split may fit no configuration;
                 # automatic choices always fit.
@@ -268,17 +271,17 @@ def test_plan_invariants(M, K, N):
                 assert s == min(split, 1 << (nkb.bit_length() - 1))
             assert ch in ((4, 8) if N > 16 else (4, 8, 11, 16))
             assert stg in (1, 2) and (variant == 0 or stg == variant)
-            assert stg == 1 or ch == 16
+            assert stg == 1 or ch in (11, 16)
 
 
 def test_plan_argument_errors():
     L = binding.lib()
     a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     ok = ctypes.byref(binding.SpmmOpts(0, 0))
-    assert L.us_spmm_plan(32, 128, 8, ok, None, ctypes.byref(b), ctypes.byref(c)) == -1
-    assert L.us_spmm_plan(40, 128, 8, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
-    assert L.us_spmm_plan(32, 128, 33, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
+    assert L.us_spmm_plan(32, 128, 8, 0, ok, None, ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(40, 128, 8, 0, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
+    assert L.us_spmm_plan(32, 128, 33, 1, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
     bad = ctypes.byref(binding.SpmmOpts(3, 0))
-    assert L.us_spmm_plan(32, 128, 8, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(32, 128, 8, 0, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
     bad = ctypes.byref(binding.SpmmOpts(0, 5))
-    assert L.us_spmm_plan(32, 128, 8, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(32, 128, 8, 1, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
