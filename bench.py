@@ -49,6 +49,7 @@ KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_09291_amd", "csrc", f)
 # row reordering.
 COPY_FACTOR = {"FETCH_SIZE": 0.5, "WRITE_SIZE": 1.0}
 MEASURED_TRAFFIC = {
+    ("ffn_down_4096x11008_s50", 8, False): dict(src="48c7adef2f7aa178", FETCH_SIZE=11375.3, WRITE_SIZE=256.0),
 }
 
 
