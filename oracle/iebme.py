@@ -19,7 +19,11 @@ Readings taken where the paper is silent:
     word L // 64 of its LT at bit L % 64 (leftmost column = least significant);
   * offsets are counted in INT4 values and stored as uint32, n_LT + 1 entries;
   * payload nibble n sits in byte n // 2, in the low half when n is even, as
-    4-bit two's complement; 16 zero bytes of tail padding follow the payload.
+    4-bit two's complement; 16 zero bytes of tail padding follow the payload;
+  * a signed b-bit quantizer (Section V-A) covers [-2^(b-1), 2^(b-1) - 1]; with
+    b = 2 (the W2A4 setting of the evaluation) the payload packs four values
+    per byte, value n at bits 2 (n mod 4) .. 2 (n mod 4) + 1 of byte n // 4,
+    everything else (mask, offsets in values, stream order) unchanged.
 """
 from __future__ import annotations
 
@@ -29,6 +33,14 @@ import numpy as np
 
 INT4_MIN, INT4_MAX = -8, 7
 TAIL_PAD_BYTES = 16
+VALUE_BITS = (4, 2)                     # W4A4 and W2A4 payloads
+
+
+def value_range(bits: int):
+    """Alphabet bounds of the signed b-bit quantizer."""
+    if bits not in VALUE_BITS:
+        raise ValueError(f"payload values are 4 or 2 bits, not {bits}")
+    return -(1 << (bits - 1)), (1 << (bits - 1)) - 1
 
 
 @dataclass
@@ -43,9 +55,10 @@ class Encoded:
     ca: int
     bitmaps: np.ndarray   # uint64, words_per_lt words per LT ("Union Bitmaps")
     offsets: np.ndarray   # uint32, n_lt + 1 entries ("Union Value Offsets")
-    payload: np.ndarray   # uint8, packed INT4 ("Compressed Values") + tail pad
+    payload: np.ndarray   # uint8, packed b-bit values ("Compressed Values") + tail pad
     P: np.ndarray         # int64 per LT: P_t = ||B_t||_0
     nnz: int
+    bits: int = 4         # bits per payload value
 
     @property
     def Q(self) -> int:
@@ -69,12 +82,13 @@ class Encoded:
         return hb * kb // 64
 
 
-def check_weights(W) -> np.ndarray:
+def check_weights(W, bits: int = 4) -> np.ndarray:
     W = np.asarray(W)
+    lo, hi = value_range(bits)
     if W.ndim != 2 or not np.issubdtype(W.dtype, np.integer):
         raise ValueError("W must be a 2-D integer matrix")
-    if W.size and (W.min() < INT4_MIN or W.max() > INT4_MAX):
-        raise ValueError("W values must lie in the signed INT4 range [-8, 7]")
+    if W.size and (W.min() < lo or W.max() > hi):
+        raise ValueError(f"W values must lie in the signed {bits}-bit range [{lo}, {hi}]")
     return W.astype(np.int64)
 
 
@@ -95,9 +109,9 @@ def areas(T: np.ndarray, ra: int, ca: int) -> np.ndarray:
     return T.reshape(n_lt, ra, hb, ca, kb).transpose(0, 1, 3, 2, 4).reshape(n_lt, ra * ca, hb, kb)
 
 
-def encode(W, lt_h: int = 16, lt_w: int = 64, ra: int = 2, ca: int = 2) -> Encoded:
-    """IE-BME encoding of a masked INT4 matrix (Section V-A)."""
-    W = check_weights(W)
+def encode(W, lt_h: int = 16, lt_w: int = 64, ra: int = 2, ca: int = 2, bits: int = 4) -> Encoded:
+    """IE-BME encoding of a masked b-bit matrix (Section V-A)."""
+    W = check_weights(W, bits)
     M, K = W.shape
     if M % lt_h or K % lt_w or lt_h % ra or lt_w % ca:
         raise ValueError("shape must tile exactly into LTs and areas")
@@ -124,9 +138,9 @@ def encode(W, lt_h: int = 16, lt_w: int = 64, ra: int = 2, ca: int = 2) -> Encod
 
     # Union Bitmaps: row-major scan, leftmost bit = LSB, packed into 64-bit words.
     nbits = hb * kb
-    bits = B.reshape(n_lt, nbits // 64, 64).astype(np.uint64)
+    mask_bits = B.reshape(n_lt, nbits // 64, 64).astype(np.uint64)
     shifts = np.arange(64, dtype=np.uint64)
-    words = np.bitwise_or.reduce(bits << shifts, axis=2)
+    words = np.bitwise_or.reduce(mask_bits << shifts, axis=2)
     bitmaps = words.reshape(-1).astype(np.uint64)
 
     # Compressed Values: compact rank rho_t(i, j) = active entries before (i, j)
@@ -142,7 +156,39 @@ def encode(W, lt_h: int = 16, lt_w: int = 64, ra: int = 2, ca: int = 2) -> Encod
     cv[addr.ravel()] = vals.ravel()
 
     return Encoded(M, K, lt_h, lt_w, ra, ca, bitmaps, offsets.astype(np.uint32),
-                   pack_nibbles(cv), P, int(np.count_nonzero(W)))
+                   pack_values(cv, bits), P, int(np.count_nonzero(W)), bits)
+
+
+def pack_values(v: np.ndarray, bits: int) -> np.ndarray:
+    """b-bit values -> bytes: value n at bits b (n mod 8/b) of byte n // (8/b).
+
+    Adds the zeroed tail pad; values are stored as b-bit two's complement.
+    """
+    if bits == 4:
+        return pack_nibbles(v)
+    value_range(bits)
+    per = 8 // bits
+    v = np.asarray(v, dtype=np.int64)
+    u = (v & ((1 << bits) - 1)).astype(np.uint8)
+    out = np.zeros(-(-v.size // per) + TAIL_PAD_BYTES, dtype=np.uint8)
+    for k in range(per):
+        part = u[k::per]
+        out[: part.size] |= (part << (bits * k)).astype(np.uint8)
+    return out
+
+
+def unpack_values(b: np.ndarray, n: int, bits: int) -> np.ndarray:
+    """Inverse of pack_values for the first n values (sign-extended to int64)."""
+    if bits == 4:
+        return unpack_nibbles(b, n)
+    value_range(bits)
+    per = 8 // bits
+    b = np.asarray(b, dtype=np.uint8)[: -(-n // per)].astype(np.int64)
+    u = np.empty(b.size * per, dtype=np.int64)
+    for k in range(per):
+        u[k::per] = (b >> (bits * k)) & ((1 << bits) - 1)
+    u = u[:n]
+    return np.where(u >= (1 << (bits - 1)), u - (1 << bits), u)
 
 
 def pack_nibbles(v: np.ndarray) -> np.ndarray:
@@ -191,7 +237,7 @@ def decode(enc: Encoded) -> np.ndarray:
     off = enc.offsets.astype(np.int64)
     if not np.array_equal(off[1:] - off[:-1], Q * P):
         raise ValueError("offsets disagree with the union bitmaps")
-    cv = unpack_nibbles(enc.payload, int(off[-1]))
+    cv = unpack_values(enc.payload, int(off[-1]), enc.bits)
     rho = np.cumsum(B, axis=1) - B
     A = np.zeros((n_lt, Q, hb * kb), dtype=np.int64)
     t_idx, pos = np.nonzero(B)
@@ -243,7 +289,7 @@ def lspd_decode_tile(enc: Encoded, t: int, G: int) -> np.ndarray:
     Bt = union_mask(enc)[t]
     Pt = int(Bt.sum())
     o = int(enc.offsets[t])
-    cv = unpack_nibbles(enc.payload, int(enc.offsets[-1]))
+    cv = unpack_values(enc.payload, int(enc.offsets[-1]), enc.bits)
     streams = [cv[o + q * Pt: o + (q + 1) * Pt] for q in range(enc.Q)]
     A = np.zeros((enc.Q, hb, kb), dtype=np.int64)
     for r in range(hb):
@@ -262,7 +308,7 @@ def lspd_decode_tile(enc: Encoded, t: int, G: int) -> np.ndarray:
 # Payload-to-Metadata Ratio (Eq. 1) and effective compute intensity (Eq. 2).
 # --------------------------------------------------------------------------
 
-def pmr_report(enc: Encoded, N: int = 0, bytes_per_weight: float = 0.5) -> dict:
+def pmr_report(enc: Encoded, N: int = 0, bytes_per_weight: float = None) -> dict:
     """Byte accounting of an encoded matrix (Section III-B/C).
 
     Metadata = union bitmaps + one offset per LT (the sentinel offset is not
@@ -270,6 +316,8 @@ def pmr_report(enc: Encoded, N: int = 0, bytes_per_weight: float = 0.5) -> dict:
     uses the stored payload, which also holds the zeros kept inside active
     groups. ``ci_eff`` is Eq. 2 evaluated as printed, for activation width N.
     """
+    if bytes_per_weight is None:
+        bytes_per_weight = enc.bits / 8                             # B_w
     n_lt = enc.n_lt
     bitmap_bytes = 8 * enc.words_per_lt * n_lt
     offset_bytes = 4 * n_lt
@@ -278,8 +326,9 @@ def pmr_report(enc: Encoded, N: int = 0, bytes_per_weight: float = 0.5) -> dict:
     payload_useful = bytes_per_weight * enc.nnz                  # B_w * M * K * (1 - s)
     payload_stored = bytes_per_weight * stored_values
     pmr = payload_useful / meta
+    per = 8 // enc.bits
     rep = dict(nnz=enc.nnz, stored_values=stored_values, n_lt=n_lt,
-               payload_stored_bytes=(stored_values + 1) // 2,
+               payload_stored_bytes=-(-stored_values // per),
                bitmap_bytes=bitmap_bytes, offset_bytes=offset_bytes, meta_bytes=meta,
                payload_useful_bytes=payload_useful, pmr=pmr,
                pmr_stored=payload_stored / meta, ci_eff=0.0)

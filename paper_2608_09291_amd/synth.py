@@ -7,7 +7,8 @@ inputs from here without sharing any of the method's code.
 Recipe (every draw from numpy PCG64):
   * seed: ``SeedSequence([20261202 + config_id, variant])``, spawned into four
     independent streams: mask, weight values, activations, scales;
-  * weight nonzeros: uniform over the 15 INT4 values {-8..-1, 1..7};
+  * weight nonzeros: uniform over the 15 INT4 values {-8..-1, 1..7}, or for
+    2-bit weights (W2A4) over the 3 values {-2, -1, 1};
   * mask: Bernoulli(keep = 1 - sparsity), i.i.d. per element; the row-skewed
     variant draws a keep rate per row from Beta(2, 3), rescales the rates to
     the requested mean and clips them to [0, 1];
@@ -87,6 +88,20 @@ def nonzero_int4(rng: np.random.Generator, shape) -> np.ndarray:
     return np.where(u < 8, u - 8, u - 7).astype(np.int8)
 
 
+def nonzero_int2(rng: np.random.Generator, shape) -> np.ndarray:
+    """Uniform draw over {-2, -1, 1} as int8."""
+    u = rng.integers(0, 3, size=shape, dtype=np.int8)
+    return np.where(u < 2, u - 2, 1).astype(np.int8)
+
+
+def _nonzero(rng, shape, bits):
+    if bits == 4:
+        return nonzero_int4(rng, shape)
+    if bits == 2:
+        return nonzero_int2(rng, shape)
+    raise ValueError(f"weights are 4 or 2 bits, not {bits}")
+
+
 def keep_mask(rng: np.random.Generator, M: int, K: int, sparsity: float,
               row_skew: bool = False, chunk_rows: int = 2048) -> np.ndarray:
     """Boolean keep mask, drawn in row chunks to bound peak memory."""
@@ -103,11 +118,11 @@ def keep_mask(rng: np.random.Generator, M: int, K: int, sparsity: float,
     return out
 
 
-def weights(w: Workload) -> np.ndarray:
-    """Masked INT4 weight matrix, int8 (M, K); zero means pruned."""
+def weights(w: Workload, bits: int = 4) -> np.ndarray:
+    """Masked INT4 (or 2-bit) weight matrix, int8 (M, K); zero means pruned."""
     mrng, vrng, _, _ = _streams(w.config_id, w.variant)
     mask = keep_mask(mrng, w.M, w.K, w.sparsity, w.row_skew)
-    vals = nonzero_int4(vrng, (w.M, w.K))
+    vals = _nonzero(vrng, (w.M, w.K), bits)
     vals[~mask] = 0
     return vals
 
@@ -128,12 +143,12 @@ def scales(w: Workload) -> np.ndarray:
 
 
 def random_problem(M: int, K: int, N: int, sparsity: float, seed: int,
-                   row_skew: bool = False):
+                   row_skew: bool = False, bits: int = 4):
     """Small seeded problem (W (M,K), Xt (N,K), scales (M,)) for parity tests."""
     ss = np.random.SeedSequence([BASE_SEED, 1000 + seed])
     mrng, vrng, xrng, srng = (np.random.Generator(np.random.PCG64(s)) for s in ss.spawn(4))
     mask = keep_mask(mrng, M, K, sparsity, row_skew)
-    W = nonzero_int4(vrng, (M, K))
+    W = _nonzero(vrng, (M, K), bits)
     W[~mask] = 0
     Xt = xrng.integers(-8, 8, size=(N, K), dtype=np.int8)
     sc = srng.uniform(0.01, 0.1, size=M).astype(np.float32)
