@@ -1,13 +1,14 @@
 #!/usr/bin/env python3
 """Benchmark of the W4A4 IE-BME SpMM on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--N n] [--split-k S] [--reorder]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--N n] [--split-k S] [--reorder] [--bits 2]
 
 One step is one us_spmm call (stream the IE-BME tiles, decode, multiply,
 combine, store Y and the dequantised Y) over one copy of the encoded weight
 matrix; the encoding itself is offline, as in the paper, and is not timed.
 With --reorder the matrix is encoded after bitmap-aware row reordering
-(Section V-B) and the kernel undoes the row permutation of every tile.
+(Section V-B) and the kernel undoes the row permutation of every tile; with
+--bits 2 the weights are 2-bit (the W2A4 setting of Section VII).
 Every timed batch queues its launches behind a bounded spin kernel, so the
 GPU runs them back to back and host launch cost never enters the event
 timings; the weight copies rotate over at least 1 GiB so that none of them
@@ -83,6 +84,7 @@ def parse():
     ap.add_argument("--N", type=int, default=0, help="activation columns (default: the workload's first)")
     ap.add_argument("--split-k", type=int, default=0)
     ap.add_argument("--reorder", action="store_true", help="row-reorder the LTs before encoding")
+    ap.add_argument("--bits", type=int, default=4, choices=(4, 2), help="weight bits (4: W4A4, 2: W2A4)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extras", action="store_true", help="skip the read-ceiling and dense GEMM points")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -131,10 +133,10 @@ class Timer:
         return total
 
 
-def spmm_bench(torch, args, w, N, timer, reorder=False):
-    W = synth.weights(w)
+def spmm_bench(torch, args, w, N, timer, reorder=False, bits=4):
+    W = synth.weights(w, bits)
     Xt = synth.activations(w, N)
-    enc = binding.encode(W, reorder=reorder)
+    enc = binding.encode(W, reorder=reorder, bits=bits)
     rep = binding.pmr(enc, N)
     dev0 = binding.to_device(enc)
     enc_bytes = dev0.nbytes
@@ -142,7 +144,7 @@ def spmm_bench(torch, args, w, N, timer, reorder=False):
     copies = [dev0] + [binding.DeviceEncoded(dev0.bitmaps.clone(), dev0.offsets.clone(),
                                              dev0.payload.clone(), dev0.M, dev0.K, dev0.n_lt,
                                              dev0.n_payload,
-                                             None if dev0.perm is None else dev0.perm.clone())
+                                             None if dev0.perm is None else dev0.perm.clone(), dev0.bits)
                        for _ in range(n_copies - 1)]
     xp = torch.from_numpy(binding.pack_int4(Xt)).cuda()
     y = torch.empty((N, w.M), dtype=torch.int32, device="cuda")
@@ -213,13 +215,13 @@ def dense_gemm(torch, w, N, steps, timer):
     return ms / steps, nbytes + w.K * N + w.M * N * 4
 
 
-def cpu_baseline(w, W, Xt, enc_bytes_alg, budget_s=12.0):
+def cpu_baseline(w, W, Xt, enc_bytes_alg, budget_s=12.0, bits=4):
     """The oracle's int64 masked dense product, timed on this host's cores."""
     from oracle import iebme, product
     product.build(force=False)
     threads = product.max_threads()
     t0 = time.perf_counter()
-    ref = iebme.encode(W)
+    ref = iebme.encode(W, bits=bits)
     dense = iebme.decode(ref).astype(np.int8)
     t_dec = time.perf_counter() - t0
     times = []
@@ -270,7 +272,10 @@ def main():
     timer = Timer(torch)
 
     log(f"[bench] workload {w.name} M={w.M} K={w.K} N={N} s={w.sparsity} dequant={w.dequant}")
-    r = spmm_bench(torch, args, w, N, timer, reorder=args.reorder)
+    if args.bits == 2 and args.reorder:
+        print("--reorder applies to 4-bit weights only", file=sys.stderr)
+        sys.exit(2)
+    r = spmm_bench(torch, args, w, N, timer, reorder=args.reorder, bits=args.bits)
     ms_step = r["ms"] / args.steps
     us = ms_step * 1e3
     gbs = r["alg_bytes"] / (ms_step * 1e-3) / 1e9
@@ -292,11 +297,11 @@ def main():
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(w, r["W"], r["Xt"], r["alg_bytes"])
+        cpu = cpu_baseline(w, r["W"], r["Xt"], r["alg_bytes"], bits=args.bits)
         log(f"[bench] cpu oracle {cpu['ms_per_call']} ms/call on {cpu['cores']} threads")
 
     rep = r["rep"]
-    plan = binding.spmm_plan(w.M, w.K, N, args.split_k, reordered=args.reorder)
+    plan = binding.spmm_plan(w.M, w.K, N, args.split_k, reordered=args.reorder, bits=args.bits)
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -311,9 +316,10 @@ def main():
         "dtype": "int8",
         "data": "synthetic",
         "config": {"workload": w.name, "M": w.M, "K": w.K, "N": N, "sparsity": w.sparsity,
-                   "dequant": w.dequant, "reordered": args.reorder, "split_k": plan[0], "chunk_lts": plan[1],
+                   "dequant": w.dequant, "weight_bits": args.bits, "reordered": args.reorder,
+                   "split_k": plan[0], "chunk_lts": plan[1],
                    "staging": "ring" if plan[2] == 2 else "whole", "plan": "auto" if not args.split_k else "forced",
-                   "weights": "w4a4 IE-BME (16x64 tiles, 2x2 areas), int8 MFMA, int32 accumulate",
+                   "weights": f"w{args.bits}a4 IE-BME (16x64 tiles, 2x2 areas), int8 MFMA, int32 accumulate",
                    "rotating_copies": r["n_copies"]},
         "us_per_call": round(us, 3),
         "dense_equiv_tops": round(tops, 2),
@@ -323,7 +329,7 @@ def main():
         "ci_eff_eq2": round(rep["ci_eff"], 3),
         "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(w.name, N, args.reorder),
+                     "traffic": measured_traffic(w.name, N, args.reorder) if args.bits == 4 else None,
                      "kernel": "us_spmm_kernel",
                      "bytes_per_launch": r["alg_bytes"]},
         "cpu_baseline": cpu,

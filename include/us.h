@@ -60,6 +60,11 @@ typedef enum {
  * row-major) is area q's value at (i, j); value n is the low nibble of byte
  * n / 2 when n is even, the high nibble when odd, in two's complement.
  *
+ * With bits = 2 (W2A4, us_encode_w2) the weights are signed 2-bit values in
+ * [-2, 1] and payload value n sits at bits 2 (n mod 4) .. 2 (n mod 4) + 1 of
+ * byte n / 4; the bitmaps, the offsets (still counted in values) and the
+ * stream order are those of the 4-bit format.
+ *
  * Row reordering (Section V-B) is recorded in `perm`. When it is NULL the
  * LTs keep their row order. Otherwise bits 4p .. 4p + 3 of perm[t] hold
  * pi_t[p], the row of LT t that was moved to row p before encoding. The
@@ -75,11 +80,12 @@ typedef struct {
     int64_t n_lt;                 /* (M/16) * (K/64)                        */
     int64_t nnz;                  /* nonzero weights                        */
     int64_t n_payload;            /* stored INT4 values = offsets[n_lt]     */
-    int64_t payload_bytes;        /* ceil(n_payload / 2) + US_PAYLOAD_PAD   */
+    int64_t payload_bytes;        /* ceil(n_payload bits / 8) + US_PAYLOAD_PAD */
     uint64_t *bitmaps;            /* n_lt * 4 words                         */
     uint32_t *offsets;            /* n_lt + 1 entries                       */
     uint8_t *payload;             /* payload_bytes bytes, zeroed padding    */
     uint64_t *perm;               /* NULL, or n_lt row permutations         */
+    int32_t bits;                 /* bits per payload value: 4, or 2 (W2A4) */
 } us_iebme;
 
 /*
@@ -92,6 +98,13 @@ typedef struct {
  * Returns US_ERR_ARG, US_ERR_SHAPE, US_ERR_RANGE or US_ERR_NOMEM on failure.
  */
 us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out);
+
+/*
+ * us_encode_w2 - IE-BME encoding of a masked signed 2-bit matrix, the W2A4
+ * setting of the evaluation (Section VII): as us_encode, with weights in
+ * [-2, 1] (US_ERR_RANGE otherwise) packed four to a byte; out->bits = 2.
+ */
+us_status us_encode_w2(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out);
 
 /*
  * us_encode_reordered - bitmap-aware row reordering followed by IE-BME
@@ -113,13 +126,13 @@ void us_iebme_free(us_iebme *m);
 /*
  * Byte accounting of an encoded matrix (Section III-B, Eq. 1; Section III-C,
  * Eq. 2). Metadata is bitmaps (32 B per LT) plus offsets (4 B per LT; the
- * sentinel is not counted). B_w = 1/2 byte for INT4.
+ * sentinel is not counted). B_w = bits / 8 bytes per weight.
  */
 typedef struct {
     int64_t nnz;                  /* nonzero weights                           */
     int64_t stored_values;        /* n_payload: nnz plus zeros of active groups */
     int64_t n_lt;
-    int64_t payload_stored_bytes; /* ceil(stored_values / 2)                   */
+    int64_t payload_stored_bytes; /* ceil(stored_values bits / 8)              */
     int64_t bitmap_bytes;         /* 32 n_lt                                   */
     int64_t offset_bytes;         /* 4 n_lt                                    */
     int64_t meta_bytes;           /* Stor_meta of Eq. 1                        */
@@ -141,12 +154,14 @@ us_status us_pmr(const us_iebme *m, int32_t N, us_pmr_report *out);
 typedef struct {
     const uint64_t *bitmaps;      /* device, n_lt * 4 words, 8-byte aligned  */
     const uint32_t *offsets;      /* device, n_lt + 1 entries, 4-byte aligned */
-    const uint8_t *payload;       /* device, ceil(n_payload / 2) + US_PAYLOAD_PAD bytes */
+    const uint8_t *payload;       /* device, ceil(n_payload bits / 8) + US_PAYLOAD_PAD bytes */
     int32_t M, K;
     int64_t n_lt, n_payload;
     const uint64_t *perm;         /* device, n_lt words, 8-byte aligned, or NULL
                                      (see us_iebme); words that are not
                                      permutations give unspecified Y       */
+    int32_t bits;                 /* 4 (0 reads as 4) or 2; 2-bit matrices
+                                     cannot be row-reordered (US_ERR_ARG)  */
 } us_iebme_dev;
 
 typedef struct {
@@ -162,12 +177,12 @@ typedef struct {
  * us_spmm_plan - the launch configuration us_spmm would use for this shape
  * and options on the current device (a 256-CU MI355X when no device is
  * visible): K slices per 16-row block (one wavefront each), LTs per chunk,
- * and payload staging (1 whole chunk, 2 ring). `reordered` != 0 plans for a
- * matrix with row permutations (us_iebme_dev.perm != NULL), whose stages
- * are larger. Host only; for tuning and reporting. Same argument errors as
+ * and payload staging (1 whole chunk, 2 ring), for a matrix of `bits`-bit
+ * values (4 or 2) that is row-reordered when `reordered` != 0 (its stages
+ * are larger). Host only; for tuning and reporting. Same argument errors as
  * us_spmm; US_ERR_ARG if no configuration fits.
  */
-us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t reordered, const us_spmm_opts *opts,
+us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t bits, int32_t reordered, const us_spmm_opts *opts,
                        int32_t *split_k, int32_t *chunk_lts, int32_t *staging);
 
 /*
@@ -182,7 +197,8 @@ us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, const us_spmm_
  * INT32 accumulation (Section VI, "UnionSparse Kernel" algorithm: the kernel
  * takes the IE-BME matrix, the activations and a split-K count, and returns Y).
  *   w      : encoded matrix, device arrays; with w->perm the LTs are
- *            row-reordered (Section V-B) and Y is still in original row order
+ *            row-reordered (Section V-B) and Y is still in original row order;
+ *            w->bits = 2 multiplies a W2A4 matrix
  *   x      : device, N x K row-major INT4, two values per byte along K
  *            (even k in the low nibble), 16-byte aligned
  *   N      : 1..32 activation columns

@@ -24,7 +24,7 @@ N_MAX = 32
 K_MAX = 130048
 
 #: Every symbol the two public headers declare.
-EXPORTS = ("us_encode", "us_encode_reordered", "us_iebme_free", "us_pmr", "us_spmm_plan", "us_spmm_workspace_size", "us_spmm",
+EXPORTS = ("us_encode", "us_encode_w2", "us_encode_reordered", "us_iebme_free", "us_pmr", "us_spmm_plan", "us_spmm_workspace_size", "us_spmm",
            "us_gemm_i8", "us_status_string", "us_probe_read", "us_probe_read_sink_words",
            "us_probe_copy", "us_probe_spin")
 
@@ -44,7 +44,7 @@ class IEBME(ctypes.Structure):
                 ("bitmaps", ctypes.POINTER(ctypes.c_uint64)),
                 ("offsets", ctypes.POINTER(ctypes.c_uint32)),
                 ("payload", ctypes.POINTER(ctypes.c_uint8)),
-                ("perm", ctypes.POINTER(ctypes.c_uint64))]
+                ("perm", ctypes.POINTER(ctypes.c_uint64)), ("bits", ctypes.c_int32)]
 
 
 class PMRReport(ctypes.Structure):
@@ -59,7 +59,8 @@ class PMRReport(ctypes.Structure):
 class IEBMEDev(ctypes.Structure):
     _fields_ = [("bitmaps", ctypes.c_void_p), ("offsets", ctypes.c_void_p),
                 ("payload", ctypes.c_void_p), ("M", ctypes.c_int32), ("K", ctypes.c_int32),
-                ("n_lt", ctypes.c_int64), ("n_payload", ctypes.c_int64), ("perm", ctypes.c_void_p)]
+                ("n_lt", ctypes.c_int64), ("n_payload", ctypes.c_int64), ("perm", ctypes.c_void_p),
+                ("bits", ctypes.c_int32)]
 
 
 class SpmmOpts(ctypes.Structure):
@@ -79,13 +80,14 @@ def lib():
         vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
         L.us_encode.argtypes = [vp, i32, i32, i64, ctypes.POINTER(IEBME)]
         L.us_encode_reordered.argtypes = [vp, i32, i32, i64, ctypes.POINTER(IEBME)]
+        L.us_encode_w2.argtypes = [vp, i32, i32, i64, ctypes.POINTER(IEBME)]
         L.us_iebme_free.argtypes = [ctypes.POINTER(IEBME)]
         L.us_iebme_free.restype = None
         L.us_pmr.argtypes = [ctypes.POINTER(IEBME), i32, ctypes.POINTER(PMRReport)]
         L.us_spmm_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(SpmmOpts),
                                              ctypes.POINTER(sz)]
         pi32 = ctypes.POINTER(i32)
-        L.us_spmm_plan.argtypes = [i32, i32, i32, i32, ctypes.POINTER(SpmmOpts), pi32, pi32, pi32]
+        L.us_spmm_plan.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(SpmmOpts), pi32, pi32, pi32]
         L.us_spmm.argtypes = [ctypes.POINTER(IEBMEDev), vp, i32, vp, vp, vp, vp, sz,
                               ctypes.POINTER(SpmmOpts), vp]
         L.us_gemm_i8.argtypes = [vp, vp, i32, i32, i32, vp, vp]
@@ -96,7 +98,7 @@ def lib():
         L.us_probe_read_sink_words.restype = sz
         L.us_probe_copy.argtypes = [vp, vp, sz, vp]
         L.us_probe_spin.argtypes = [ctypes.c_uint64, vp]
-        for name in ("us_encode", "us_encode_reordered", "us_pmr", "us_spmm_workspace_size", "us_spmm_plan", "us_spmm", "us_gemm_i8",
+        for name in ("us_encode", "us_encode_w2", "us_encode_reordered", "us_pmr", "us_spmm_workspace_size", "us_spmm_plan", "us_spmm", "us_gemm_i8",
                      "us_probe_read", "us_probe_copy", "us_probe_spin"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -134,6 +136,9 @@ class Encoded:
     def n_payload(self): return self._s.n_payload
 
     @property
+    def bits(self): return self._s.bits
+
+    @property
     def bitmaps(self) -> np.ndarray:
         return np.ctypeslib.as_array(self._s.bitmaps, shape=(4 * self._s.n_lt,))
 
@@ -166,13 +171,15 @@ class Encoded:
             pass
 
 
-def encode(W: np.ndarray, reorder: bool = False) -> Encoded:
-    """us_encode (or us_encode_reordered) on a host int8 matrix (values in [-8, 7])."""
+def encode(W: np.ndarray, reorder: bool = False, bits: int = 4) -> Encoded:
+    """us_encode, us_encode_reordered or (bits = 2) us_encode_w2 on a host int8 matrix."""
     W = np.ascontiguousarray(W, dtype=np.int8)
     if W.ndim != 2:
         raise ValueError("W must be 2-D")
+    if bits == 2 and reorder:
+        raise ValueError("2-bit matrices are not row-reordered")
     s = IEBME()
-    name = "us_encode_reordered" if reorder else "us_encode"
+    name = "us_encode_w2" if bits == 2 else "us_encode_reordered" if reorder else "us_encode"
     _check(name, getattr(lib(), name)(W.ctypes.data, W.shape[0], W.shape[1], W.shape[1],
                                       ctypes.byref(s)))
     return Encoded(s)
@@ -207,16 +214,17 @@ class DeviceEncoded:
     n_lt: int
     n_payload: int
     perm: "object" = None
+    bits: int = 4
 
     def struct(self) -> IEBMEDev:
         return IEBMEDev(self.bitmaps.data_ptr(), self.offsets.data_ptr(), self.payload.data_ptr(),
                         self.M, self.K, self.n_lt, self.n_payload,
-                        None if self.perm is None else self.perm.data_ptr())
+                        None if self.perm is None else self.perm.data_ptr(), self.bits)
 
     @property
     def nbytes(self) -> int:
         """Encoded bytes the kernel streams: bitmaps, offsets, stored payload, row permutations."""
-        return (32 * self.n_lt + 4 * (self.n_lt + 1) + (self.n_payload + 1) // 2
+        return (32 * self.n_lt + 4 * (self.n_lt + 1) + (self.n_payload * self.bits + 7) // 8
                 + (0 if self.perm is None else 8 * self.n_lt))
 
 
@@ -226,7 +234,7 @@ def to_device(enc: Encoded, device="cuda") -> DeviceEncoded:
     off = torch.from_numpy(enc.offsets.view(np.int32).copy()).to(device)
     pay = torch.from_numpy(enc.payload.copy()).to(device)
     perm = None if enc.perm is None else torch.from_numpy(enc.perm.view(np.int64).copy()).to(device)
-    return DeviceEncoded(bm, off, pay, enc.M, enc.K, enc.n_lt, enc.n_payload, perm)
+    return DeviceEncoded(bm, off, pay, enc.M, enc.K, enc.n_lt, enc.n_payload, perm, enc.bits)
 
 
 def pack_int4(Xt: np.ndarray) -> np.ndarray:
@@ -244,11 +252,12 @@ def workspace_size(M: int, K: int, N: int, split_k: int = 0) -> int:
     return n.value
 
 
-def spmm_plan(M: int, K: int, N: int, split_k: int = 0, variant: int = 0, reordered: bool = False):
+def spmm_plan(M: int, K: int, N: int, split_k: int = 0, variant: int = 0, reordered: bool = False,
+              bits: int = 4):
     """us_spmm_plan: (K slices per row block, LTs per chunk, staging 1 whole / 2 ring)."""
     opts = SpmmOpts(split_k, variant)
     a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
-    _check("us_spmm_plan", lib().us_spmm_plan(M, K, N, int(bool(reordered)), ctypes.byref(opts),
+    _check("us_spmm_plan", lib().us_spmm_plan(M, K, N, bits, int(bool(reordered)), ctypes.byref(opts),
                                               ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
     return a.value, b.value, c.value
 

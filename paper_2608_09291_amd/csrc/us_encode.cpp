@@ -108,7 +108,7 @@ private:
     uint32_t gen_ = 0;
 };
 
-us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool reorder, us_iebme *out);
+us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool reorder, int bits, us_iebme *out);
 
 }  // namespace
 
@@ -126,28 +126,33 @@ extern "C" const char *us_status_string(us_status s) {
 }
 
 extern "C" us_status us_encode(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out) {
-    return encode_impl(w, M, K, ldw, false, out);
+    return encode_impl(w, M, K, ldw, false, 4, out);
+}
+
+extern "C" us_status us_encode_w2(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out) {
+    return encode_impl(w, M, K, ldw, false, 2, out);
 }
 
 extern "C" us_status us_encode_reordered(const int8_t *w, int32_t M, int32_t K, int64_t ldw, us_iebme *out) {
-    return encode_impl(w, M, K, ldw, true, out);
+    return encode_impl(w, M, K, ldw, true, 4, out);
 }
 
 namespace {
 
-us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool reorder, us_iebme *out) {
+us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool reorder, int bits, us_iebme *out) {
     if (!w || !out) return US_ERR_ARG;
     if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W) return US_ERR_SHAPE;
     if (ldw < K) return US_ERR_ARG;
     if ((uint64_t)M * (uint64_t)K >= (1ull << 32)) return US_ERR_SHAPE;
 
-    // Every weight must be a signed INT4 value.
+    // Every weight must be a signed `bits`-bit value.
+    const int lo = -(1 << (bits - 1)), hi = (1 << (bits - 1)) - 1;
     std::atomic<bool> bad{false};
     parallel_ranges(M, [&](int64_t r0, int64_t r1) {
         for (int64_t r = r0; r < r1 && !bad.load(std::memory_order_relaxed); ++r) {
             const int8_t *row = w + r * ldw;
             for (int32_t k = 0; k < K; ++k)
-                if (row[k] < -8 || row[k] > 7) { bad = true; break; }
+                if (row[k] < lo || row[k] > hi) { bad = true; break; }
         }
     });
     if (bad) return US_ERR_RANGE;
@@ -253,7 +258,8 @@ us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool r
     }
     offsets[n_lt] = (uint32_t)run;   // run <= M * K < 2^32
 
-    const int64_t payload_bytes = (int64_t)((run + 1) / 2) + US_PAYLOAD_PAD;
+    const int per_byte = 8 / bits;                        // values per payload byte
+    const int64_t payload_bytes = (int64_t)((run + per_byte - 1) / per_byte) + US_PAYLOAD_PAD;
     uint8_t *payload = (uint8_t *)std::calloc((size_t)payload_bytes, 1);
     if (!payload) {
         std::free(bitmaps);
@@ -263,8 +269,9 @@ us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool r
     }
 
     // Pass 2: Compressed Values, CV[o_t + q P_t + rho] = W_t^(q)(i, j) for
-    // every active (i, j), zeros of active groups included. Each LT starts on
-    // a multiple of four values, so LTs never share a byte.
+    // every active (i, j), zeros of active groups included; value n takes
+    // bits (n mod per_byte) * bits of byte n / per_byte. Each LT starts on a
+    // multiple of four values, so LTs never share a byte.
     parallel_ranges(n_lt, [&](int64_t t0, int64_t t1) {
         for (int64_t t = t0; t < t1; ++t) {
             const int8_t *rows[US_LT_H];
@@ -278,8 +285,8 @@ us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool r
                 const int i = L / kAreaW, j = L % kAreaW;
                 for (int q = 0; q < US_RA * US_CA; ++q) {
                     const uint64_t n = o + (uint64_t)q * Pt + rho;
-                    const uint8_t nib = (uint8_t)area_value(rows, q, i, j) & 0xF;
-                    payload[n >> 1] |= (uint8_t)(nib << ((n & 1) * 4));
+                    const uint8_t v = (uint8_t)area_value(rows, q, i, j) & (uint8_t)((1 << bits) - 1);
+                    payload[n / per_byte] |= (uint8_t)(v << ((n % per_byte) * bits));
                 }
                 ++rho;
             }
@@ -300,6 +307,7 @@ us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool r
     out->offsets = offsets;
     out->payload = payload;
     out->perm = perm;
+    out->bits = bits;
     return US_OK;
 }
 
@@ -334,13 +342,15 @@ extern "C" us_status us_pmr(const us_iebme *m, int32_t N, us_pmr_report *out) {
     if ((int64_t)m->offsets[n_lt] != m->n_payload) return US_ERR_FORMAT;
     if (m->nnz < 0 || m->nnz > m->n_payload) return US_ERR_FORMAT;
 
-    const double bw = 0.5;   // bytes per INT4 weight
+    const int bits = m->bits == 0 ? 4 : m->bits;
+    if (bits != 4 && bits != 2) return US_ERR_FORMAT;
+    const double bw = bits / 8.0;   // bytes per weight (B_w)
     us_pmr_report r;
     std::memset(&r, 0, sizeof(r));
     r.nnz = m->nnz;
     r.stored_values = m->n_payload;
     r.n_lt = n_lt;
-    r.payload_stored_bytes = (m->n_payload + 1) / 2;
+    r.payload_stored_bytes = (m->n_payload * bits + 7) / 8;
     r.bitmap_bytes = 8 * US_WORDS_PER_LT * n_lt;
     r.offset_bytes = 4 * n_lt;
     r.meta_bytes = r.bitmap_bytes + r.offset_bytes;

@@ -25,8 +25,10 @@ bool aligned(const void *ptr, uintptr_t n) { return ((uintptr_t)ptr % n) == 0; }
 // chunks. Residency: LDS, and at most 16 wavefronts per CU (the kernel's
 // registers). wpg_only > 0 fixes the number of wavefronts; staging 1 or 2
 // allows linear or ring payload staging only (0: either). perm: the LTs are
-// row-reordered (their stages hold two more per-LT arrays).
-void choose_config(int M, int K, int N, bool perm, int n_cu, int wpg_only, int staging, int &wpg, int &cfg) {
+// row-reordered (their stages hold two more per-LT arrays); bits: payload
+// value width (2-bit chunks stage half the payload bytes).
+void choose_config(int M, int K, int N, bool perm, int bits, int n_cu, int wpg_only, int staging, int &wpg,
+                   int &cfg) {
     const int nrb = M / 16, nkb = K / 64;
     long best[5] = {0, 0, 0, 0, 0};
     wpg = 0;
@@ -40,7 +42,7 @@ void choose_config(int M, int K, int N, bool perm, int n_cu, int wpg_only, int s
         for (int idx = 0; idx < kNumCfgs; ++idx) {
             if (!cfg_allowed(idx, N) || (staging == 1 && kCfgs[idx].ring) || (staging == 2 && !kCfgs[idx].ring))
                 continue;
-            const int lds = lds_bytes(idx, N, w, perm);
+            const int lds = lds_bytes(idx, N, w, perm, bits);
             if (lds > kMaxLds) continue;
             const int c = kCfgs[idx].ch;
             const int per_cu = max(1, min(kMaxLds / lds, 16 / w));      // resident workgroups per CU
@@ -79,9 +81,11 @@ int device_cus() {
 
 }  // namespace
 
-extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t reordered, const us_spmm_opts *opts,
-                                  int32_t *split_k, int32_t *chunk_lts, int32_t *staging) {
+extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t bits, int32_t reordered,
+                                  const us_spmm_opts *opts, int32_t *split_k, int32_t *chunk_lts, int32_t *staging) {
     if (!split_k || !chunk_lts || !staging) return US_ERR_ARG;
+    if (bits != 4 && bits != 2) return US_ERR_ARG;
+    if (bits == 2 && reordered) return US_ERR_ARG;
     if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
     if (N < 1 || N > US_N_MAX) return US_ERR_SHAPE;
     int wpg_only = 0, stg = 0;
@@ -96,7 +100,7 @@ extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t reord
         }
     }
     int wpg = 0, cfg = -1;
-    choose_config(M, K, N, reordered != 0, device_cus(), wpg_only, stg, wpg, cfg);
+    choose_config(M, K, N, reordered != 0, bits, device_cus(), wpg_only, stg, wpg, cfg);
     if (cfg < 0) return US_ERR_ARG;
     *split_k = wpg;
     *chunk_lts = kCfgs[cfg].ch;
@@ -133,6 +137,9 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
         (scale && (!aligned(scale, 4) || !aligned(y_f32, 4))) || (w->perm && !aligned(w->perm, 8)))
         return US_ERR_ARG;
     const bool perm = w->perm != nullptr;
+    const int bits = w->bits == 0 ? 4 : w->bits;
+    if (bits != 4 && bits != 2) return US_ERR_FORMAT;
+    if (bits == 2 && perm) return US_ERR_ARG;              // no reordered 2-bit kernels
 
     int wpg_only = 0, staging = 0;
     if (opts) {
@@ -146,7 +153,7 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
         }
     }
     int wpg = 0, cfg = -1;
-    choose_config(M, K, N, perm, device_cus(), wpg_only, staging, wpg, cfg);
+    choose_config(M, K, N, perm, bits, device_cus(), wpg_only, staging, wpg, cfg);
     if (cfg < 0) return US_ERR_ARG;                        // no configuration fits LDS
 
     SpmmArgs a;
@@ -156,7 +163,7 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     // Whole 16-byte pieces: a piece is either fully inside the range or fully
     // outside it (then it reads zeros). Rounding up stays within the
     // US_PAYLOAD_PAD bytes that follow the payload.
-    a.pay_bytes = (int32_t)((((w->n_payload + 1) / 2) + 15) & ~(int64_t)15);
+    a.pay_bytes = (int32_t)((((w->n_payload * bits + 7) / 8) + 15) & ~(int64_t)15);
     a.x = x;
     a.y = y;
     a.scale = scale;
@@ -168,6 +175,8 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     a.nkb = (int32_t)nkb;
 
     hipStream_t s = (hipStream_t)stream;
-    const hipError_t err = perm ? launch_cfg_perm(wpg, cfg, a, s) : launch_cfg<false>(wpg, cfg, a, s);
+    const hipError_t err = bits == 2 ? launch_cfg_w2(wpg, cfg, a, s)
+                           : perm    ? launch_cfg_perm(wpg, cfg, a, s)
+                                     : launch_cfg<false, 4>(wpg, cfg, a, s);
     return err == hipSuccess ? US_OK : US_ERR_DEVICE;
 }

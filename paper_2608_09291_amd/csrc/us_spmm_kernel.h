@@ -53,6 +53,9 @@
 //    activations are expanded to bytes that hold the value in the high
 //    nibble (16 v, exact in int8), so the MFMA sums are 256 Y; the epilogue
 //    shifts right by 8. |256 Y| <= 256 * 64 * K < 2^31 for K <= US_K_MAX.
+//    2-bit weights (BITS = 2, the W2A4 setting of Section VII) go to the top
+//    two bits of a byte (64 v): the sums are 1024 Y, |1024 Y| <= 1024 * 16 K
+//    < 2^31, and the epilogue shifts by 10.
 //    Both operands put the even and the odd positions of each 8-group in
 //    separate dwords, the same slot order on both sides of the product.
 #ifndef UNIONSPARSE_US_SPMM_KERNEL_H
@@ -109,15 +112,16 @@ __device__ inline u32x2 perm_selectors(uint32_t m) {
 //   payload : the chunk's compressed values, streamed from the 16-byte
 //             boundary at or below the chunk's first byte (up to 15 bytes
 //             early); a segment window may read 8 bytes past the last value,
-//             so a chunk needs at most 32 CH + 2 pieces of 16 bytes.
+//             so a chunk needs at most 8 BITS CH + 2 pieces of 16 bytes (an
+//             LT holds at most 1024 values).
 //             Linear staging (RING = false) keeps the whole chunk. RING =
 //             true keeps a ring of four 1 KB slots (stream byte b in slot
 //             (b / 1024) mod 4), so the stage does not grow with CH: an LT
-//             spans at most 528 bytes with its window overhang, so the four
-//             slots hold every LT that is ready for decoding. The 160 bytes
-//             after the ring repeat its first 160 bytes, so windows that start
-//             past the end of the ring (by at most one stream, 128 bytes,
-//             plus a window) read on into it;
+//             spans at most 128 BITS + 16 bytes with its window overhang, so
+//             the four slots hold every LT that is ready for decoding. The
+//             160 bytes after the ring repeat its first 160 bytes, so windows
+//             that start past the end of the ring (by at most one stream,
+//             32 BITS bytes, plus a window) read on into it;
 //   bitmaps : union-mask rows, 8 dwords per LT;
 //             (this and the next three arrays have room for a whole number
 //             of 4-LT passes; entries past the chunk are never decoded)
@@ -133,9 +137,9 @@ __device__ inline u32x2 perm_selectors(uint32_t m) {
 //             each activation column; rows are 16 bytes longer than the
 //             slice so that the 16 rows read by one instruction fall in
 //             different LDS banks.
-template <int CH, bool RING, bool PERM>
+template <int CH, bool RING, bool PERM, int BITS>
 struct Chunk {
-    static constexpr int kPayPieces = 32 * CH + 2;
+    static constexpr int kPayPieces = 8 * BITS * CH + 2;
     static constexpr int kLoads = (kPayPieces + 63) / 64;     // payload loads per lane
     static constexpr int kRing = 4096;                        // ring: four 1 KB slots
     static constexpr int kGuard = 160;                        // copy of the ring's first bytes
@@ -223,20 +227,40 @@ __device__ __forceinline__ int2 place(uint32_t w, uint2 sel) {
                      (int32_t)__builtin_amdgcn_perm(hi, lo, sel.y));
 }
 
+// Eight packed 2-bit values (the low 16 bits of w) -> the two slot dwords
+// of one segment, each value in the top two bits of its byte (64 v). Byte j
+// of x takes nibble j of w (values 2j, 2j + 1 in its bits 0..3; its high
+// nibble is never used), then the odd and even values move to bits 6..7 of
+// byte j, which is where place() finds ranks 2j + 1 and 2j.
+__device__ __forceinline__ int2 place2(uint32_t w, uint2 sel) {
+    const uint32_t x = __builtin_amdgcn_perm(w >> 4, w, 0x05010400u);
+    const uint32_t hi = (x << 4) & 0xC0C0C0C0u;
+    const uint32_t lo = (x << 6) & 0xC0C0C0C0u;
+    return make_int2((int32_t)__builtin_amdgcn_perm(hi, lo, sel.x),
+                     (int32_t)__builtin_amdgcn_perm(hi, lo, sel.y));
+}
+
 // Decode one LT into the MFMA A operand of this lane.
 //   mrow : union-mask row i of the LT
 //   base : LDS bit address of row i's first value in area stream 2a
 //   sd   : bits of one area stream (stream 2a + 1 starts sd bits later)
 //   rot  : (8 g - 3) mod 32, so that rotating mrow right by it puts the
 //          lane's segment at bits 3..10 (the selector table's byte offset)
+template <int BITS>
 __device__ __forceinline__ i32x4 decode_tile(const u32x2 *lut, uint32_t mrow, uint32_t base, uint32_t sd,
                                              uint32_t lomask, uint32_t rot) {
-    const uint32_t bn0 = base + 4u * __popc(mrow & lomask);
+    const uint32_t bn0 = base + (uint32_t)BITS * __popc(mrow & lomask);
     const uint32_t bn1 = bn0 + sd;
     const u32x2 sv = *(const u32x2 *)((const char *)lut + (__builtin_amdgcn_alignbit(mrow, mrow, rot) & 0x7F8u));
     const uint2 sel = make_uint2(sv.x, sv.y);
-    const int2 c0 = place(window(bn0), sel);
-    const int2 c1 = place(window(bn1), sel);
+    int2 c0, c1;
+    if constexpr (BITS == 4) {
+        c0 = place(window(bn0), sel);
+        c1 = place(window(bn1), sel);
+    } else {
+        c0 = place2(window(bn0), sel);
+        c1 = place2(window(bn1), sel);
+    }
     return (i32x4){c0.x, c0.y, c1.x, c1.y};
 }
 
@@ -251,13 +275,16 @@ __device__ __forceinline__ i32x4 unpack_x(uint2 x) {
 // MULTI: some slices take several chunks (their inputs are then requested
 // one chunk ahead); otherwise every slice is a single chunk. RING: the
 // payload is staged in a 4 KB ring instead of whole (see Chunk). PERM: the
-// LTs were row-reordered and p.perm32 holds their permutations. The host's
+// LTs were row-reordered and p.perm32 holds their permutations. BITS: bits
+// per payload value (4, or 2 for W2A4). The host's
 // configuration choice assumes four resident wavefronts per SIMD, i.e. at
 // most 128 VGPRs: PERM variants are held to that explicitly (their
 // multi-chunk forms would take up to 144), the others stay under it.
-template <int WPG, int NB, int CH, bool MULTI, bool RING, bool PERM>
+template <int WPG, int NB, int CH, bool MULTI, bool RING, bool PERM, int BITS>
 __global__ __launch_bounds__(64 * WPG, PERM ? 4 : 1) void us_spmm_kernel(SpmmArgs p, int stage_bytes) {
-    using C = Chunk<CH, RING, PERM>;
+    using C = Chunk<CH, RING, PERM, BITS>;
+    static_assert(BITS == 4 || BITS == 2, "payload values are 4 or 2 bits");
+    constexpr int kValShift = BITS == 4 ? 1 : 2;          // log2(values per byte)
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
     __shared__ u32x2 lut[256];                               // selector table
     const uint32_t lds0 = (uint32_t)(size_t)(lds_u32 *)lds;  // LDS address of the dynamic block
@@ -360,8 +387,8 @@ __global__ __launch_bounds__(64 * WPG, PERM ? 4 : 1) void us_spmm_kernel(SpmmArg
         wait_vm_all();                                     // offsets, bitmaps, activations
 
         const uint32_t ob = lane_value(offv, 0), oe = lane_value(offv, cnt);
-        A0 = (ob >> 1) & ~15u;                             // first staged payload byte
-        const uint32_t span = (((oe - 2u * A0) >> 3) << 2) + 8u;
+        A0 = (ob >> kValShift) & ~15u;                     // first staged payload byte
+        const uint32_t span = ((((oe - (A0 << kValShift)) * (uint32_t)BITS) >> 5) << 2) + 8u;
         const uint32_t nq = min((span + 15u) >> 4, (uint32_t)C::kPayPieces);
         // Payload: 16-byte pieces from A0; load u brings stage bytes
         // [1024 u, 1024 u + 1024). Pieces past the chunk read zero (range
@@ -409,8 +436,8 @@ __global__ __launch_bounds__(64 * WPG, PERM ? 4 : 1) void us_spmm_kernel(SpmmArg
         // popcounts of the rows before i. With PERM the row base and the
         // mask row of (i, a), i.e. of reordered row 8a + i, go to the lane
         // row of original row r = pi[8a + i]: 2 (r mod 8) + r / 8.
-        // Payload value v of the matrix is stream bit 4 v - 8 A0, at LDS bit
-        // address 8 st + (4 v - 8 A0), taken mod 32768 with the ring.
+        // Payload value v of the matrix is stream bit BITS v - 8 A0, at LDS
+        // bit address 8 st + (BITS v - 8 A0), taken mod 32768 with the ring.
         const uint32_t rmask = RING ? 0x7FFFu : ~0u;
         {
             const uint32_t jj = (uint32_t)lane >> 4;
@@ -434,7 +461,7 @@ __global__ __launch_bounds__(64 * WPG, PERM ? 4 : 1) void us_spmm_kernel(SpmmArg
                 ex += dpp_row<0x112>(ex);
                 ex += dpp_row<0x114>(ex);
                 ex += dpp_row<0x118>(ex);
-                const uint32_t bval = 8u * st + ((4u * (o[ps].x + ex) - 8u * A0) & rmask);
+                const uint32_t bval = 8u * st + (((uint32_t)BITS * (o[ps].x + ex) - 8u * A0) & rmask);
                 lds_store(p_base + 256 * ps, bval);
                 if constexpr (PERM) {
                     // This lane's own lane row is written first, so that a
@@ -446,12 +473,13 @@ __global__ __launch_bounds__(64 * WPG, PERM ? 4 : 1) void us_spmm_kernel(SpmmArg
                     lds_store(q_base + 256 * ps + slot, bval);
                     lds_store(q_base + 256 * ps + slot + C::kRowDelta, mrow[ps]);
                 }
-                if (rr == 0) lds_store(p_sd + 16 * ps, o[ps].y - o[ps].x);
+                if (rr == 0) lds_store(p_sd + 16 * ps, ((o[ps].y - o[ps].x) * (uint32_t)BITS) >> 2);
             }
         }
         // LT k can be decoded once the pieces holding its windows have landed:
-        // o_{k+1} - 2 A0 + 16 <= 2048 (u + 1), i.e. after load u = need_k.
-        const uint32_t need = (lds_load(st_off + 4 * min(lane + 1, CH)) - 2u * A0 + 15u) >> 11;
+        // BITS o_{k+1} - 8 A0 + 64 <= 8192 (u + 1) stream bits, i.e. after
+        // load u = need_k.
+        const uint32_t need = ((uint32_t)BITS * lds_load(st_off + 4 * min(lane + 1, CH)) - 8u * A0 + 63u) >> 13;
 
         // LDS addresses of the next LT's mask row, row base, stream length and
         // activations for this lane; they advance as LTs are decoded. The
@@ -469,7 +497,7 @@ __global__ __launch_bounds__(64 * WPG, PERM ? 4 : 1) void us_spmm_kernel(SpmmArg
             const uint32_t mrow = lds_load(row_at(0));
             const uint32_t base = lds_load(a_base);
             const uint32_t sd = lds_load(a_sd);
-            const i32x4 A = decode_tile(lut, mrow, base, sd, lomask, rot);
+            const i32x4 A = decode_tile<BITS>(lut, mrow, base, sd, lomask, rot);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
                 acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, unpack_x(x_pair(a_x[nb])), acc[nb], 0, 0, 0);
@@ -483,8 +511,8 @@ __global__ __launch_bounds__(64 * WPG, PERM ? 4 : 1) void us_spmm_kernel(SpmmArg
             const uint32_t m0 = lds_load(row_at(0)), m1 = lds_load(row_at(1));
             const uint32_t b0 = lds_load(a_base), b1 = lds_load(a_base + 64);
             const uint2 sd = lds_load2(a_sd);
-            const i32x4 A0v = decode_tile(lut, m0, b0, sd.x, lomask, rot);
-            const i32x4 A1v = decode_tile(lut, m1, b1, sd.y, lomask, rot);
+            const i32x4 A0v = decode_tile<BITS>(lut, m0, b0, sd.x, lomask, rot);
+            const i32x4 A1v = decode_tile<BITS>(lut, m1, b1, sd.y, lomask, rot);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
                 acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0v, unpack_x(x_pair(a_x[nb])), acc[nb], 0, 0, 0);
@@ -558,7 +586,7 @@ __global__ __launch_bounds__(64 * WPG, PERM ? 4 : 1) void us_spmm_kernel(SpmmArg
         int32_t s = 0;
 #pragma unroll
         for (int w = 0; w < WPG; ++w) s += (int32_t)lds_load(lds0 + (uint32_t)(w * stage_bytes) + idx);
-        const int32_t yv = s >> 8;                            // exact: s = 256 Y
+        const int32_t yv = s >> (BITS == 4 ? 8 : 10);         // exact: s = 256 Y (1024 Y)
         const int64_t m = (int64_t)mb * 16 + r;
         const int64_t M = p.M;
         p.y[n * M + m] = yv;
@@ -577,71 +605,76 @@ constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 inline bool cfg_allowed(int idx, int N) { return N <= 16 || (kCfgs[idx].ch <= 8 && !kCfgs[idx].ring); }
 
-template <int CH, bool RING, bool PERM>
-int stage_bytes(int N) { return (Chunk<CH, RING, PERM>::bytes(N) + 15) & ~15; }
+template <int CH, bool RING, bool PERM, int BITS>
+int stage_bytes(int N) { return (Chunk<CH, RING, PERM, BITS>::bytes(N) + 15) & ~15; }
 
-template <bool PERM>
+template <bool PERM, int BITS>
 int lds_bytes_t(int idx, int N, int wpg) {
     int st = 0;
     switch (idx) {
-        case 0: st = stage_bytes<4, false, PERM>(N); break;
-        case 1: st = stage_bytes<8, false, PERM>(N); break;
-        case 2: st = stage_bytes<11, false, PERM>(N); break;
-        case 3: st = stage_bytes<16, false, PERM>(N); break;
-        case 4: st = stage_bytes<16, true, PERM>(N); break;
-        default: st = stage_bytes<11, true, PERM>(N); break;
+        case 0: st = stage_bytes<4, false, PERM, BITS>(N); break;
+        case 1: st = stage_bytes<8, false, PERM, BITS>(N); break;
+        case 2: st = stage_bytes<11, false, PERM, BITS>(N); break;
+        case 3: st = stage_bytes<16, false, PERM, BITS>(N); break;
+        case 4: st = stage_bytes<16, true, PERM, BITS>(N); break;
+        default: st = stage_bytes<11, true, PERM, BITS>(N); break;
     }
     return kLutBytes + wpg * st;
 }
 
-inline int lds_bytes(int idx, int N, int wpg, bool perm) {
-    return perm ? lds_bytes_t<true>(idx, N, wpg) : lds_bytes_t<false>(idx, N, wpg);
+inline int lds_bytes(int idx, int N, int wpg, bool perm, int bits) {
+    if (bits == 2) return perm ? lds_bytes_t<true, 2>(idx, N, wpg) : lds_bytes_t<false, 2>(idx, N, wpg);
+    return perm ? lds_bytes_t<true, 4>(idx, N, wpg) : lds_bytes_t<false, 4>(idx, N, wpg);
 }
 
-template <int WPG, int NB, int CH, bool RING, bool PERM>
+template <int WPG, int NB, int CH, bool RING, bool PERM, int BITS>
 hipError_t launch_spmm(const SpmmArgs &a, hipStream_t s) {
     const bool multi = (a.nkb + WPG - 1) / WPG > CH;
-    auto kern = multi ? us_spmm_kernel<WPG, NB, CH, true, RING, PERM> : us_spmm_kernel<WPG, NB, CH, false, RING, PERM>;
+    auto kern = multi ? us_spmm_kernel<WPG, NB, CH, true, RING, PERM, BITS>
+                      : us_spmm_kernel<WPG, NB, CH, false, RING, PERM, BITS>;
     // Allow more than 64 KB of dynamic LDS (set once per instantiation).
     static const hipError_t attr =
-        (hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, true, RING, PERM>,
+        (hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, true, RING, PERM, BITS>,
                              hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes),
-         hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, false, RING, PERM>,
+         hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, false, RING, PERM, BITS>,
                              hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes));
     (void)attr;
-    const int st = stage_bytes<CH, RING, PERM>(a.N);
+    const int st = stage_bytes<CH, RING, PERM, BITS>(a.N);
     hipLaunchKernelGGL(kern, dim3(a.M / 16), dim3(64 * WPG), WPG * st, s, a, st);
     return hipGetLastError();
 }
 
-template <int NB, int CH, bool RING, bool PERM>
+template <int NB, int CH, bool RING, bool PERM, int BITS>
 hipError_t launch_spmm_wpg(int wpg, const SpmmArgs &a, hipStream_t s) {
     switch (wpg) {
-        case 1: return launch_spmm<1, NB, CH, RING, PERM>(a, s);
-        case 2: return launch_spmm<2, NB, CH, RING, PERM>(a, s);
-        case 4: return launch_spmm<4, NB, CH, RING, PERM>(a, s);
-        case 8: return launch_spmm<8, NB, CH, RING, PERM>(a, s);
-        default: return launch_spmm<16, NB, CH, RING, PERM>(a, s);
+        case 1: return launch_spmm<1, NB, CH, RING, PERM, BITS>(a, s);
+        case 2: return launch_spmm<2, NB, CH, RING, PERM, BITS>(a, s);
+        case 4: return launch_spmm<4, NB, CH, RING, PERM, BITS>(a, s);
+        case 8: return launch_spmm<8, NB, CH, RING, PERM, BITS>(a, s);
+        default: return launch_spmm<16, NB, CH, RING, PERM, BITS>(a, s);
     }
 }
 
 // Launch configuration idx of kCfgs with wpg wavefronts per workgroup.
-template <bool PERM>
+template <bool PERM, int BITS>
 hipError_t launch_cfg(int wpg, int idx, const SpmmArgs &a, hipStream_t s) {
     if (a.N > 16)
-        return idx == 1 ? launch_spmm_wpg<2, 8, false, PERM>(wpg, a, s) : launch_spmm_wpg<2, 4, false, PERM>(wpg, a, s);
+        return idx == 1 ? launch_spmm_wpg<2, 8, false, PERM, BITS>(wpg, a, s)
+                        : launch_spmm_wpg<2, 4, false, PERM, BITS>(wpg, a, s);
     switch (idx) {
-        case 5: return launch_spmm_wpg<1, 11, true, PERM>(wpg, a, s);
-        case 4: return launch_spmm_wpg<1, 16, true, PERM>(wpg, a, s);
-        case 3: return launch_spmm_wpg<1, 16, false, PERM>(wpg, a, s);
-        case 2: return launch_spmm_wpg<1, 11, false, PERM>(wpg, a, s);
-        case 1: return launch_spmm_wpg<1, 8, false, PERM>(wpg, a, s);
-        default: return launch_spmm_wpg<1, 4, false, PERM>(wpg, a, s);
+        case 5: return launch_spmm_wpg<1, 11, true, PERM, BITS>(wpg, a, s);
+        case 4: return launch_spmm_wpg<1, 16, true, PERM, BITS>(wpg, a, s);
+        case 3: return launch_spmm_wpg<1, 16, false, PERM, BITS>(wpg, a, s);
+        case 2: return launch_spmm_wpg<1, 11, false, PERM, BITS>(wpg, a, s);
+        case 1: return launch_spmm_wpg<1, 8, false, PERM, BITS>(wpg, a, s);
+        default: return launch_spmm_wpg<1, 4, false, PERM, BITS>(wpg, a, s);
     }
 }
 
-// The PERM instantiations live in their own translation unit.
+// The row-reordered (4-bit) and the 2-bit instantiations live in their own
+// translation units.
 hipError_t launch_cfg_perm(int wpg, int idx, const SpmmArgs &a, hipStream_t s);
+hipError_t launch_cfg_w2(int wpg, int idx, const SpmmArgs &a, hipStream_t s);
 
 }  // namespace us_spmm_detail
 

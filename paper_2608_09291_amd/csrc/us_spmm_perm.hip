@@ -6,7 +6,7 @@
 namespace us_spmm_detail {
 
 hipError_t launch_cfg_perm(int wpg, int idx, const SpmmArgs &a, hipStream_t s) {
-    return launch_cfg<true>(wpg, idx, a, s);
+    return launch_cfg<true, 4>(wpg, idx, a, s);
 }
 
 }  // namespace us_spmm_detail

@@ -163,7 +163,8 @@ def _dev_struct(M=32, K=128, n_lt=None, n_payload=0, ptr=0x1000):
     ("null_w", -1), ("null_x", -1), ("null_y", -1), ("scale_without_yf", -1),
     ("m_not_16", -2), ("k_not_64", -2), ("k_too_big", -2), ("n_zero", -2), ("n_33", -2),
     ("n_lt_wrong", -6), ("payload_odd", -6), ("payload_too_big", -6),
-    ("split_3", -1), ("variant", -1), ("misaligned_x", -1), ("misaligned_perm", -1)])
+    ("split_3", -1), ("variant", -1), ("misaligned_x", -1), ("misaligned_perm", -1),
+    ("bits_3", -6), ("bits_2_reordered", -1)])
 def test_spmm_argument_errors_before_launch(case, status):
     """Every argument error returns before touching the GPU (pointers are fake)."""
     L = binding.lib()
@@ -205,6 +206,10 @@ def test_spmm_argument_errors_before_launch(case, status):
         x = 0x2002
     elif case == "misaligned_perm":
         w.perm = 0x5004
+    elif case == "bits_3":
+        w.bits = 3
+    elif case == "bits_2_reordered":
+        w.bits, w.perm = 2, 0x5000
     got = L.us_spmm(wp, x, N, y, sc, yf, None, 0, ctypes.byref(opts), None)
     assert got == status
 
@@ -278,10 +283,12 @@ def test_plan_argument_errors():
     L = binding.lib()
     a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     ok = ctypes.byref(binding.SpmmOpts(0, 0))
-    assert L.us_spmm_plan(32, 128, 8, 0, ok, None, ctypes.byref(b), ctypes.byref(c)) == -1
-    assert L.us_spmm_plan(40, 128, 8, 0, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
-    assert L.us_spmm_plan(32, 128, 33, 1, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
+    assert L.us_spmm_plan(32, 128, 8, 4, 0, ok, None, ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(40, 128, 8, 4, 0, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
+    assert L.us_spmm_plan(32, 128, 33, 4, 1, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
     bad = ctypes.byref(binding.SpmmOpts(3, 0))
-    assert L.us_spmm_plan(32, 128, 8, 0, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(32, 128, 8, 4, 0, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
     bad = ctypes.byref(binding.SpmmOpts(0, 5))
-    assert L.us_spmm_plan(32, 128, 8, 1, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(32, 128, 8, 4, 1, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(32, 128, 8, 3, 0, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(32, 128, 8, 2, 1, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1

@@ -32,11 +32,11 @@ def announce(msg):
     sys.stderr.flush()
 
 
-def run_spmm(torch, W, Xt, scale=None, split_k=0, dev=None, variant=0, reorder=False):
+def run_spmm(torch, W, Xt, scale=None, split_k=0, dev=None, variant=0, reorder=False, bits=4):
     M, K = W.shape
     N = Xt.shape[0]
     if dev is None:
-        dev = binding.to_device(binding.encode(W, reorder=reorder))
+        dev = binding.to_device(binding.encode(W, reorder=reorder, bits=bits))
     xp = torch.from_numpy(binding.pack_int4(Xt)).cuda()
     y = torch.full((N, M), SENTINEL, dtype=torch.int32, device="cuda")
     sc = yf = None
