@@ -44,7 +44,9 @@ typedef enum {
 #define US_CA 2             /* C_A: area columns per LT (Q = R_A C_A = 4)  */
 #define US_WORDS_PER_LT 4   /* 8 x 32 union-mask bits = four 64-bit words  */
 #define US_PAYLOAD_PAD 16   /* zero bytes after the payload                */
-#define US_N_MAX 32         /* widest activation matrix                    */
+#define US_N_MAX 32         /* widest activation matrix of one kernel pass */
+#define US_N_LIMIT 1024     /* widest activation matrix; N > US_N_MAX runs as
+                               slabs of US_N_MAX columns, each streaming W */
 #define US_K_MAX 130048     /* K bound: int32 headroom of the kernel's scaled sums */
 
 /*
@@ -177,7 +179,8 @@ typedef struct {
  * us_spmm_plan - the launch configuration us_spmm would use for this shape
  * and options on the current device (a 256-CU MI355X when no device is
  * visible): K slices per 16-row block (one wavefront each), LTs per chunk,
- * and payload staging (1 whole chunk, 2 ring), for a matrix of `bits`-bit
+ * and payload staging (1 whole chunk, 2 ring) of the first slab of
+ * min(N, US_N_MAX) columns, for a matrix of `bits`-bit
  * values (4 or 2) that is row-reordered when `reordered` != 0 (its stages
  * are larger). Host only; for tuning and reporting. Same argument errors as
  * us_spmm; US_ERR_ARG if no configuration fits.
@@ -201,7 +204,10 @@ us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, const us_spmm_
  *            w->bits = 2 multiplies a W2A4 matrix
  *   x      : device, N x K row-major INT4, two values per byte along K
  *            (even k in the low nibble), 16-byte aligned
- *   N      : 1..32 activation columns
+ *   N      : 1..US_N_LIMIT activation columns; beyond US_N_MAX (32) the
+ *            call runs one pass per slab of 32 columns (the last one
+ *            narrower), each with its own configuration and each reading W
+ *            again: prefill-sized N at decode-kernel cost per slab
  *   y      : device int32, N x M row-major (y[n * M + m] = Y[m][n])
  *   scale  : device float32[M] or NULL; with it, y_f32[n * M + m] =
  *            fl32(fl32(Y[m][n]) * scale[m]) is written too (the dequant
@@ -223,7 +229,8 @@ us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N, int32_t *y
  *   w : device int8, M x K row-major, 16-byte aligned
  *   x : device int8, N x K row-major (row n is activation column n), 16-byte aligned
  *   y : device int32, N x M row-major
- * M % 16 == 0, K % 64 == 0, K <= US_K_MAX, 1 <= N <= 32.
+ * M % 16 == 0, K % 64 == 0, K <= US_K_MAX, 1 <= N <= US_N_LIMIT (slabs of 32
+ * columns beyond 32, as in us_spmm).
  */
 us_status us_gemm_i8(const int8_t *w, const int8_t *x, int32_t M, int32_t K, int32_t N,
                      int32_t *y, void *stream);

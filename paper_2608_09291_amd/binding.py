@@ -20,7 +20,8 @@ US_OK = 0
 STATUS = {0: "US_OK", -1: "US_ERR_ARG", -2: "US_ERR_SHAPE", -3: "US_ERR_RANGE",
           -4: "US_ERR_NOMEM", -5: "US_ERR_DEVICE", -6: "US_ERR_FORMAT"}
 PAYLOAD_PAD = 16
-N_MAX = 32
+N_MAX = 32          # widest single kernel pass
+N_LIMIT = 1024      # widest activation matrix (slabs of N_MAX beyond N_MAX)
 K_MAX = 130048
 
 #: Every symbol the two public headers declare.

@@ -157,16 +157,23 @@ extern "C" us_status us_gemm_i8(const int8_t *w, const int8_t *x, int32_t M, int
                                 int32_t *y, void *stream) {
     if (!w || !x || !y) return US_ERR_ARG;
     if (M <= 0 || K <= 0 || M % 16 || K % 64 || K > US_K_MAX) return US_ERR_SHAPE;
-    if (N < 1 || N > US_N_MAX) return US_ERR_SHAPE;
+    if (N < 1 || N > US_N_LIMIT) return US_ERR_SHAPE;
     if (!aligned16(w) || !aligned16(x) || ((uintptr_t)y & 3)) return US_ERR_ARG;
     const int nrb = M / 16, nkb = K / 64;
     int wpg = 1;
     while (wpg < 16 && nrb * wpg * 2 <= 256 * 16) wpg *= 2;
     while (wpg > 1 && wpg > nkb) wpg /= 2;
     hipStream_t s = (hipStream_t)stream;
-    const hipError_t err = N > 16 ? launch_gemm_wpg<2>(wpg, w, x, y, M, K, N, s)
-                                  : launch_gemm_wpg<1>(wpg, w, x, y, M, K, N, s);
-    return err == hipSuccess ? US_OK : US_ERR_DEVICE;
+    // Slabs of up to US_N_MAX columns, as in us_spmm.
+    for (int n0 = 0; n0 < N; n0 += US_N_MAX) {
+        const int ns = N - n0 < US_N_MAX ? N - n0 : US_N_MAX;
+        const int8_t *xs = x + (int64_t)n0 * K;
+        int32_t *ys = y + (int64_t)n0 * M;
+        const hipError_t err = ns > 16 ? launch_gemm_wpg<2>(wpg, w, xs, ys, M, K, ns, s)
+                                       : launch_gemm_wpg<1>(wpg, w, xs, ys, M, K, ns, s);
+        if (err != hipSuccess) return US_ERR_DEVICE;
+    }
+    return US_OK;
 }
 
 extern "C" size_t us_probe_read_sink_words(size_t bytes) { return probe_blocks(bytes / 16); }

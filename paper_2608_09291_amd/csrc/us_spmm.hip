@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <atomic>
 
 #include "us.h"
@@ -87,7 +88,7 @@ extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t bits,
     if (bits != 4 && bits != 2) return US_ERR_ARG;
     if (bits == 2 && reordered) return US_ERR_ARG;
     if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
-    if (N < 1 || N > US_N_MAX) return US_ERR_SHAPE;
+    if (N < 1 || N > US_N_LIMIT) return US_ERR_SHAPE;
     int wpg_only = 0, stg = 0;
     if (opts) {
         if (opts->variant < 0 || opts->variant > 2) return US_ERR_ARG;
@@ -100,7 +101,7 @@ extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t bits,
         }
     }
     int wpg = 0, cfg = -1;
-    choose_config(M, K, N, reordered != 0, bits, device_cus(), wpg_only, stg, wpg, cfg);
+    choose_config(M, K, std::min(N, US_N_MAX), reordered != 0, bits, device_cus(), wpg_only, stg, wpg, cfg);
     if (cfg < 0) return US_ERR_ARG;
     *split_k = wpg;
     *chunk_lts = kCfgs[cfg].ch;
@@ -112,7 +113,7 @@ extern "C" us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, con
                                             size_t *bytes) {
     if (!bytes) return US_ERR_ARG;
     if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
-    if (N < 1 || N > US_N_MAX) return US_ERR_SHAPE;
+    if (N < 1 || N > US_N_LIMIT) return US_ERR_SHAPE;
     if (opts && (opts->variant < 0 || opts->variant > 2 || opts->split_k < 0)) return US_ERR_ARG;
     *bytes = 0;
     return US_OK;
@@ -128,7 +129,7 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     const int32_t M = w->M, K = w->K;
     if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
     if ((uint64_t)M * (uint64_t)K >= (1ull << 32)) return US_ERR_SHAPE;
-    if (N < 1 || N > US_N_MAX) return US_ERR_SHAPE;
+    if (N < 1 || N > US_N_LIMIT) return US_ERR_SHAPE;
     const int64_t nkb = K / US_LT_W;
     if (w->n_lt != (int64_t)(M / US_LT_H) * nkb) return US_ERR_FORMAT;
     if (w->n_payload < 0 || w->n_payload > (int64_t)M * K || w->n_payload % 4) return US_ERR_FORMAT;
@@ -152,9 +153,15 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
             while (wpg_only > nkb) wpg_only /= 2;          // at least one LT per slice
         }
     }
-    int wpg = 0, cfg = -1;
-    choose_config(M, K, N, perm, bits, device_cus(), wpg_only, staging, wpg, cfg);
-    if (cfg < 0) return US_ERR_ARG;                        // no configuration fits LDS
+    // Slabs of up to US_N_MAX columns: every full slab shares one
+    // configuration, a narrower last slab gets its own. Both are chosen
+    // before anything is launched.
+    const int n_cu = device_cus();
+    const int n_full = std::min<int>(N, US_N_MAX), n_last = N % US_N_MAX == 0 ? n_full : N % US_N_MAX;
+    int wpg = 0, cfg = -1, wpg_last = 0, cfg_last = -1;
+    choose_config(M, K, n_full, perm, bits, n_cu, wpg_only, staging, wpg, cfg);
+    choose_config(M, K, n_last, perm, bits, n_cu, wpg_only, staging, wpg_last, cfg_last);
+    if (cfg < 0 || cfg_last < 0) return US_ERR_ARG;        // no configuration fits LDS
 
     SpmmArgs a;
     a.bm32 = (const uint32_t *)w->bitmaps;
@@ -164,19 +171,24 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     // outside it (then it reads zeros). Rounding up stays within the
     // US_PAYLOAD_PAD bytes that follow the payload.
     a.pay_bytes = (int32_t)((((w->n_payload * bits + 7) / 8) + 15) & ~(int64_t)15);
-    a.x = x;
-    a.y = y;
     a.scale = scale;
-    a.yf = y_f32;
     a.perm32 = (const uint32_t *)w->perm;
     a.M = M;
     a.K = K;
-    a.N = N;
     a.nkb = (int32_t)nkb;
 
     hipStream_t s = (hipStream_t)stream;
-    const hipError_t err = bits == 2 ? launch_cfg_w2(wpg, cfg, a, s)
-                           : perm    ? launch_cfg_perm(wpg, cfg, a, s)
-                                     : launch_cfg<false, 4>(wpg, cfg, a, s);
-    return err == hipSuccess ? US_OK : US_ERR_DEVICE;
+    for (int n0 = 0; n0 < N; n0 += US_N_MAX) {
+        const int ns = std::min(US_N_MAX, N - n0);
+        const int sw = ns == n_full ? wpg : wpg_last, sc = ns == n_full ? cfg : cfg_last;
+        a.x = x + (int64_t)n0 * (K / 2);
+        a.y = y + (int64_t)n0 * M;
+        a.yf = y_f32 ? y_f32 + (int64_t)n0 * M : nullptr;
+        a.N = ns;
+        const hipError_t err = bits == 2 ? launch_cfg_w2(sw, sc, a, s)
+                               : perm    ? launch_cfg_perm(sw, sc, a, s)
+                                         : launch_cfg<false, 4>(sw, sc, a, s);
+        if (err != hipSuccess) return US_ERR_DEVICE;
+    }
+    return US_OK;
 }

@@ -66,11 +66,20 @@ WORKLOADS = {
             note="LLaMA-2-13B FFN, row-skewed density"),
         _wl("ffn_28672x8192_s70", 4, 0, 28672, 8192, 0.7, (1, 32), dequant=True,
             note="70B-class FFN, whole matrix on one GPU"),
+        _wl("ffn_28672x8192_s40", 4, 1, 28672, 8192, 0.4, (8,), dequant=True,
+            note="the paper's 28672x8192 shape at 40% sparsity (its PMR example)"),
+        _wl("prof_28672x7168_s50", 5, 0, 28672, 7168, 0.5, (8,),
+            note="the paper's first profiling shape (m=28672, k=7168, batch 8)"),
+        _wl("prof_12288x49152_s50", 5, 1, 12288, 49152, 0.5, (4,),
+            note="the paper's second profiling shape (m=12288, k=49152, batch 4)"),
     ]
 }
 
-#: Largest activation width drawn; narrower N take the leading columns.
+#: Activation columns drawn from the workload's own stream; narrower N take
+#: the leading columns, wider N (prefill, up to N_LIMIT) append columns from
+#: a second stream so that the first 32 never change.
 N_DRAW = 32
+N_LIMIT = 1024
 
 
 def _streams(config_id: int, variant: int):
@@ -129,11 +138,15 @@ def weights(w: Workload, bits: int = 4) -> np.ndarray:
 
 def activations(w: Workload, N: int) -> np.ndarray:
     """INT4 activations as int8 of shape (N, K): row n is activation column n."""
-    if not 1 <= N <= N_DRAW:
-        raise ValueError(f"N={N} outside [1, {N_DRAW}]")
+    if not 1 <= N <= N_LIMIT:
+        raise ValueError(f"N={N} outside [1, {N_LIMIT}]")
     _, _, xrng, _ = _streams(w.config_id, w.variant)
     xt = xrng.integers(-8, 8, size=(N_DRAW, w.K), dtype=np.int8)
-    return np.ascontiguousarray(xt[:N])
+    if N <= N_DRAW:
+        return np.ascontiguousarray(xt[:N])
+    more = np.random.Generator(np.random.PCG64(np.random.SeedSequence([BASE_SEED + w.config_id, w.variant, 1])))
+    extra = more.integers(-8, 8, size=(N - N_DRAW, w.K), dtype=np.int8)
+    return np.ascontiguousarray(np.concatenate([xt, extra]))
 
 
 def scales(w: Workload) -> np.ndarray:

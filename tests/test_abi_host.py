@@ -161,7 +161,7 @@ def _dev_struct(M=32, K=128, n_lt=None, n_payload=0, ptr=0x1000):
 
 @pytest.mark.parametrize("case,status", [
     ("null_w", -1), ("null_x", -1), ("null_y", -1), ("scale_without_yf", -1),
-    ("m_not_16", -2), ("k_not_64", -2), ("k_too_big", -2), ("n_zero", -2), ("n_33", -2),
+    ("m_not_16", -2), ("k_not_64", -2), ("k_too_big", -2), ("n_zero", -2), ("n_1025", -2),
     ("n_lt_wrong", -6), ("payload_odd", -6), ("payload_too_big", -6),
     ("split_3", -1), ("variant", -1), ("misaligned_x", -1), ("misaligned_perm", -1),
     ("bits_3", -6), ("bits_2_reordered", -1)])
@@ -190,8 +190,8 @@ def test_spmm_argument_errors_before_launch(case, status):
         w.n_lt = 2048
     elif case == "n_zero":
         N = 0
-    elif case == "n_33":
-        N = 33
+    elif case == "n_1025":
+        N = 1025
     elif case == "n_lt_wrong":
         w.n_lt += 1
     elif case == "payload_odd":
@@ -218,7 +218,7 @@ def test_gemm_argument_errors():
     L = binding.lib()
     assert L.us_gemm_i8(None, 0x10, 16, 64, 1, 0x20, None) == -1
     assert L.us_gemm_i8(0x10, 0x10, 17, 64, 1, 0x20, None) == -2
-    assert L.us_gemm_i8(0x10, 0x10, 16, 64, 33, 0x20, None) == -2
+    assert L.us_gemm_i8(0x10, 0x10, 16, 64, 1025, 0x20, None) == -2
     assert L.us_gemm_i8(0x18, 0x10, 16, 64, 1, 0x20, None) == -1
 
 
@@ -285,7 +285,7 @@ def test_plan_argument_errors():
     ok = ctypes.byref(binding.SpmmOpts(0, 0))
     assert L.us_spmm_plan(32, 128, 8, 4, 0, ok, None, ctypes.byref(b), ctypes.byref(c)) == -1
     assert L.us_spmm_plan(40, 128, 8, 4, 0, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
-    assert L.us_spmm_plan(32, 128, 33, 4, 1, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
+    assert L.us_spmm_plan(32, 128, 1025, 4, 1, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
     bad = ctypes.byref(binding.SpmmOpts(3, 0))
     assert L.us_spmm_plan(32, 128, 8, 4, 0, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
     bad = ctypes.byref(binding.SpmmOpts(0, 5))
