@@ -152,6 +152,46 @@ typedef struct {
  */
 us_status us_pmr(const us_iebme *m, int32_t N, us_pmr_report *out);
 
+/*
+ * Cross-format byte accounting (Section III-B, Eq. 1 and the PMR comparison
+ * across precisions and formats; Section III-C, Eq. 2 and the roofline view).
+ * For the sparsity pattern of an encoded matrix and a value width, each
+ * format's metadata and payload bytes:
+ *   US_FMT_DENSE       : every weight stored, no metadata;
+ *   US_FMT_CSR         : nonzeros only, a 32-bit column index per nonzero and
+ *                        M + 1 32-bit row pointers;
+ *   US_FMT_AREA_BITMAP : every 8 x 32 area of every LT with its own 256-bit
+ *                        bitmap and 32-bit payload offset (IE-BME with one
+ *                        area per mask), nonzeros only;
+ *   US_FMT_IEBME       : the union mask shared by Q = 4 areas (32 B + 4 B
+ *                        per LT), payload with the zeros of active groups.
+ */
+typedef enum { US_FMT_DENSE = 0, US_FMT_CSR = 1, US_FMT_AREA_BITMAP = 2, US_FMT_IEBME = 3 } us_format;
+#define US_NUM_FORMATS 4
+
+typedef struct {
+    int32_t format;               /* us_format                                   */
+    int32_t value_bits;           /* 16, 8, 4 or 2: B_w = value_bits / 8         */
+    int64_t meta_bytes;           /* Stor_meta of Eq. 1 (0 for dense)            */
+    double payload_useful_bytes;  /* B_w NNZ (B_w M K for dense)                 */
+    double payload_stored_bytes;  /* what the format stores as values            */
+    double pmr;                   /* Eq. 1 (0 for dense: no metadata)            */
+    double ci_eff;                /* Eq. 2 for N columns, as printed (dense: s = 0,
+                                     no metadata term)                           */
+    double total_bytes;           /* metadata + stored payload                   */
+    double ci_stored;             /* Eq. 2's form on the bytes actually stored:
+                                     2 NNZ N / (total_bytes + B_w N K), useful
+                                     MACs only (dense: all M K)                  */
+} us_format_report;
+
+/*
+ * us_pmr_formats - fill out[f] for every format f in us_format (in that
+ * order) for the mask of `m` at `value_bits` bits per value (16, 8, 4, 2)
+ * and N >= 1 activation columns. Host only. US_ERR_ARG for other widths or
+ * N < 1; US_ERR_FORMAT as us_pmr.
+ */
+us_status us_pmr_formats(const us_iebme *m, int32_t value_bits, int32_t N, us_format_report out[US_NUM_FORMATS]);
+
 /* An IE-BME matrix whose three arrays the caller has copied to the GPU. */
 typedef struct {
     const uint64_t *bitmaps;      /* device, n_lt * 4 words, 8-byte aligned  */

@@ -25,7 +25,7 @@ N_LIMIT = 1024      # widest activation matrix (slabs of N_MAX beyond N_MAX)
 K_MAX = 130048
 
 #: Every symbol the two public headers declare.
-EXPORTS = ("us_encode", "us_encode_w2", "us_encode_reordered", "us_iebme_free", "us_pmr", "us_spmm_plan", "us_spmm_workspace_size", "us_spmm",
+EXPORTS = ("us_encode", "us_encode_w2", "us_encode_reordered", "us_iebme_free", "us_pmr", "us_pmr_formats", "us_spmm_plan", "us_spmm_workspace_size", "us_spmm",
            "us_gemm_i8", "us_status_string", "us_probe_read", "us_probe_read_sink_words",
            "us_probe_copy", "us_probe_spin")
 
@@ -57,6 +57,16 @@ class PMRReport(ctypes.Structure):
                 ("ci_eff", ctypes.c_double), ("perm_bytes", ctypes.c_int64)]
 
 
+FORMATS = ("dense", "csr", "area_bitmap", "iebme")
+
+
+class FormatReport(ctypes.Structure):
+    _fields_ = [("format", ctypes.c_int32), ("value_bits", ctypes.c_int32), ("meta_bytes", ctypes.c_int64),
+                ("payload_useful_bytes", ctypes.c_double), ("payload_stored_bytes", ctypes.c_double),
+                ("pmr", ctypes.c_double), ("ci_eff", ctypes.c_double), ("total_bytes", ctypes.c_double),
+                ("ci_stored", ctypes.c_double)]
+
+
 class IEBMEDev(ctypes.Structure):
     _fields_ = [("bitmaps", ctypes.c_void_p), ("offsets", ctypes.c_void_p),
                 ("payload", ctypes.c_void_p), ("M", ctypes.c_int32), ("K", ctypes.c_int32),
@@ -85,6 +95,7 @@ def lib():
         L.us_iebme_free.argtypes = [ctypes.POINTER(IEBME)]
         L.us_iebme_free.restype = None
         L.us_pmr.argtypes = [ctypes.POINTER(IEBME), i32, ctypes.POINTER(PMRReport)]
+        L.us_pmr_formats.argtypes = [ctypes.POINTER(IEBME), i32, i32, ctypes.POINTER(FormatReport)]
         L.us_spmm_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(SpmmOpts),
                                              ctypes.POINTER(sz)]
         pi32 = ctypes.POINTER(i32)
@@ -99,7 +110,7 @@ def lib():
         L.us_probe_read_sink_words.restype = sz
         L.us_probe_copy.argtypes = [vp, vp, sz, vp]
         L.us_probe_spin.argtypes = [ctypes.c_uint64, vp]
-        for name in ("us_encode", "us_encode_w2", "us_encode_reordered", "us_pmr", "us_spmm_workspace_size", "us_spmm_plan", "us_spmm", "us_gemm_i8",
+        for name in ("us_encode", "us_encode_w2", "us_encode_reordered", "us_pmr", "us_pmr_formats", "us_spmm_workspace_size", "us_spmm_plan", "us_spmm", "us_gemm_i8",
                      "us_probe_read", "us_probe_copy", "us_probe_spin"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -190,6 +201,13 @@ def pmr(enc: Encoded, N: int = 0) -> dict:
     r = PMRReport()
     _check("us_pmr", lib().us_pmr(ctypes.byref(enc.struct()), N, ctypes.byref(r)))
     return {name: getattr(r, name) for name, _ in PMRReport._fields_}
+
+
+def pmr_formats(enc: Encoded, value_bits: int, N: int) -> dict:
+    """us_pmr_formats: {format name: report dict} for the mask of enc at value_bits bits."""
+    out = (FormatReport * len(FORMATS))()
+    _check("us_pmr_formats", lib().us_pmr_formats(ctypes.byref(enc.struct()), value_bits, N, out))
+    return {FORMATS[r.format]: {name: getattr(r, name) for name, _ in FormatReport._fields_} for r in out}
 
 
 # ---------------------------------------------------------------------------

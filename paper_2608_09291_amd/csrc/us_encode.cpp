@@ -367,3 +367,64 @@ extern "C" us_status us_pmr(const us_iebme *m, int32_t N, us_pmr_report *out) {
     *out = r;
     return US_OK;
 }
+
+extern "C" us_status us_pmr_formats(const us_iebme *m, int32_t value_bits, int32_t N,
+                                    us_format_report out[US_NUM_FORMATS]) {
+    if (!out || N < 1) return US_ERR_ARG;
+    if (value_bits != 16 && value_bits != 8 && value_bits != 4 && value_bits != 2) return US_ERR_ARG;
+    us_pmr_report base;
+    const us_status st = us_pmr(m, 0, &base);          // validates the arrays
+    if (st != US_OK) return st;
+
+    const double bw = value_bits / 8.0;                // B_w
+    const double M = m->M, K = m->K, Nd = N;
+    const double nnz = (double)m->nnz;
+    const double keep = nnz / (M * K);                 // 1 - s
+    // Eq. 2 as printed: 2 M N (1-s) / (B_w M (1-s) (1 + 1/PMR) + B_w N);
+    // with no metadata the 1/PMR term is absent.
+    auto ci = [&](double keep_, double pmr) {
+        const double inflation = pmr > 0.0 ? 1.0 + 1.0 / pmr : 1.0;
+        const double den = bw * M * keep_ * inflation + bw * Nd;
+        return den > 0.0 ? 2.0 * M * Nd * keep_ / den : 0.0;
+    };
+    const int64_t n_lt = base.n_lt;
+    for (int f = 0; f < US_NUM_FORMATS; ++f) {
+        us_format_report r;
+        std::memset(&r, 0, sizeof(r));
+        r.format = f;
+        r.value_bits = value_bits;
+        switch (f) {
+            case US_FMT_DENSE:
+                r.meta_bytes = 0;
+                r.payload_useful_bytes = bw * M * K;
+                r.payload_stored_bytes = bw * M * K;
+                r.pmr = 0.0;
+                r.ci_eff = ci(1.0, 0.0);
+                break;
+            case US_FMT_CSR:
+                r.meta_bytes = 4 * m->nnz + 4 * ((int64_t)m->M + 1);
+                r.payload_useful_bytes = bw * nnz;
+                r.payload_stored_bytes = bw * nnz;
+                break;
+            case US_FMT_AREA_BITMAP:
+                r.meta_bytes = (int64_t)(US_RA * US_CA) * (32 + 4) * n_lt;
+                r.payload_useful_bytes = bw * nnz;
+                r.payload_stored_bytes = bw * nnz;
+                break;
+            default:
+                r.meta_bytes = base.meta_bytes;
+                r.payload_useful_bytes = bw * nnz;
+                r.payload_stored_bytes = bw * (double)m->n_payload;
+                break;
+        }
+        if (f != US_FMT_DENSE) {
+            r.pmr = r.meta_bytes > 0 ? r.payload_useful_bytes / (double)r.meta_bytes : 0.0;
+            r.ci_eff = keep > 0.0 ? ci(keep, r.pmr) : 0.0;
+        }
+        r.total_bytes = (double)r.meta_bytes + r.payload_stored_bytes;
+        const double macs = f == US_FMT_DENSE ? M * K : nnz;
+        r.ci_stored = 2.0 * macs * Nd / (r.total_bytes + bw * Nd * K);
+        out[f] = r;
+    }
+    return US_OK;
+}
