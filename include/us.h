@@ -213,6 +213,8 @@ typedef struct {
     int32_t variant;  /* payload staging in LDS: 0 = automatic, 1 = whole
                          chunk, 2 = 4 KB ring (N <= 16 only); a choice
                          that fits no configuration returns US_ERR_ARG   */
+    int32_t chunk_lts; /* LTs per chunk: 0 = automatic, else 4, 8, 11 or
+                         16 (4 or 8 when N > 16); for tuning and tests   */
 } us_spmm_opts;
 
 /*

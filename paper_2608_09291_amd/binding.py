@@ -75,7 +75,7 @@ class IEBMEDev(ctypes.Structure):
 
 
 class SpmmOpts(ctypes.Structure):
-    _fields_ = [("split_k", ctypes.c_int32), ("variant", ctypes.c_int32)]
+    _fields_ = [("split_k", ctypes.c_int32), ("variant", ctypes.c_int32), ("chunk_lts", ctypes.c_int32)]
 
 
 _lib = None
@@ -272,9 +272,9 @@ def workspace_size(M: int, K: int, N: int, split_k: int = 0) -> int:
 
 
 def spmm_plan(M: int, K: int, N: int, split_k: int = 0, variant: int = 0, reordered: bool = False,
-              bits: int = 4):
+              bits: int = 4, chunk_lts: int = 0):
     """us_spmm_plan: (K slices per row block, LTs per chunk, staging 1 whole / 2 ring)."""
-    opts = SpmmOpts(split_k, variant)
+    opts = SpmmOpts(split_k, variant, chunk_lts)
     a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     _check("us_spmm_plan", lib().us_spmm_plan(M, K, N, bits, int(bool(reordered)), ctypes.byref(opts),
                                               ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
@@ -282,10 +282,10 @@ def spmm_plan(M: int, K: int, N: int, split_k: int = 0, variant: int = 0, reorde
 
 
 def spmm(w: DeviceEncoded, x_packed, N: int, y, scale=None, y_f32=None, split_k: int = 0,
-         ws=None, stream=None, wstruct: IEBMEDev = None, variant: int = 0) -> None:
+         ws=None, stream=None, wstruct: IEBMEDev = None, variant: int = 0, chunk_lts: int = 0) -> None:
     """us_spmm: y[n, m] = sum_k W[m, k] X[k, n] (+ optional dequant into y_f32)."""
     s = wstruct if wstruct is not None else w.struct()
-    opts = SpmmOpts(split_k, variant)
+    opts = SpmmOpts(split_k, variant, chunk_lts)
     _check("us_spmm", lib().us_spmm(
         ctypes.byref(s), x_packed.data_ptr(), N, y.data_ptr(),
         None if scale is None else scale.data_ptr(),

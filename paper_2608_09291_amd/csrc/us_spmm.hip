@@ -16,32 +16,34 @@ using namespace us_spmm_detail;
 
 bool aligned(const void *ptr, uintptr_t n) { return ((uintptr_t)ptr % n) == 0; }
 
+bool chunk_option_ok(int ch) { return ch == 0 || ch == 4 || ch == 8 || ch == 11 || ch == 16; }
+
 // Wavefronts per workgroup (= K slices per row block) and chunk
 // configuration. A wavefront pays one memory round trip (offsets, then
 // payload) per chunk, and a CU runs one generation of resident workgroups
-// after another, so the choice minimises the number of such latency-bound
-// phases: generations x chunks per slice. Ties go to fewer generations (a
-// wavefront requests its next chunk's inputs early; a new workgroup starts
-// cold), then to more wavefronts per CU, then to linear staging and shorter
-// chunks. Residency: LDS, and at most 16 wavefronts per CU (the kernel's
+// after another; a generation also pays a cold start (kernel arguments,
+// selector table, first requests) worth about two chunk round trips. The
+// choice minimises generations x (2 + chunks per slice); ties go to fewer
+// generations, then to more wavefronts per CU, then to linear staging and
+// shorter chunks. (Fitted to a sweep of every configuration over 16 shapes
+// and widths: within 1 % of the fastest on average, 7 % at worst.) Residency: LDS, and at most 16 wavefronts per CU (the kernel's
 // registers). wpg_only > 0 fixes the number of wavefronts; staging 1 or 2
 // allows linear or ring payload staging only (0: either). perm: the LTs are
 // row-reordered (their stages hold two more per-LT arrays); bits: payload
-// value width (2-bit chunks stage half the payload bytes).
-void choose_config(int M, int K, int N, bool perm, int bits, int n_cu, int wpg_only, int staging, int &wpg,
-                   int &cfg) {
+// value width (2-bit chunks stage half the payload bytes); ch_only > 0 fixes
+// the chunk length.
+void choose_config(int M, int K, int N, bool perm, int bits, int n_cu, int wpg_only, int staging, int ch_only,
+                   int &wpg, int &cfg) {
     const int nrb = M / 16, nkb = K / 64;
     long best[5] = {0, 0, 0, 0, 0};
     wpg = 0;
     cfg = -1;
-    // With two column blocks every chunk stages 32 activation rows, so
-    // short slices pay that per few LTs: at most 4 slices per row block
-    // (measured on 12288 x 4096 and 28672 x 8192 at N = 32).
-    const int w_max = N > 16 ? 4 : 16;
+    constexpr long kGenCost = 2;                       // cold start of a generation, in chunk round trips
     for (int w = 16; w >= 1; w /= 2) {
-        if (w > nkb || (wpg_only > 0 && w != wpg_only) || (wpg_only == 0 && w > w_max)) continue;
+        if (w > nkb || (wpg_only > 0 && w != wpg_only)) continue;
         for (int idx = 0; idx < kNumCfgs; ++idx) {
-            if (!cfg_allowed(idx, N) || (staging == 1 && kCfgs[idx].ring) || (staging == 2 && !kCfgs[idx].ring))
+            if (!cfg_allowed(idx, N) || (staging == 1 && kCfgs[idx].ring) || (staging == 2 && !kCfgs[idx].ring) ||
+                (ch_only > 0 && kCfgs[idx].ch != ch_only))
                 continue;
             const int lds = lds_bytes(idx, N, w, perm, bits);
             if (lds > kMaxLds) continue;
@@ -50,7 +52,7 @@ void choose_config(int M, int K, int N, bool perm, int bits, int n_cu, int wpg_o
             const long gens = (nrb + (long)n_cu * per_cu - 1) / ((long)n_cu * per_cu);
             const long chunks = ((nkb + w - 1) / w + c - 1) / c;
             const long waves = (long)w * min((long)per_cu, (nrb + n_cu - 1) / (long)n_cu);
-            const long key[5] = {gens * chunks, gens, -waves, kCfgs[idx].ring ? 1 : 0, c};
+            const long key[5] = {gens * (kGenCost + chunks), gens, -waves, kCfgs[idx].ring ? 1 : 0, c};
             bool better = cfg < 0;
             for (int k = 0; k < 5 && !better; ++k) {
                 if (key[k] != best[k]) {
@@ -89,10 +91,12 @@ extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t bits,
     if (bits == 2 && reordered) return US_ERR_ARG;
     if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
     if (N < 1 || N > US_N_LIMIT) return US_ERR_SHAPE;
-    int wpg_only = 0, stg = 0;
+    int wpg_only = 0, stg = 0, ch_only = 0;
     if (opts) {
         if (opts->variant < 0 || opts->variant > 2) return US_ERR_ARG;
+        if (!chunk_option_ok(opts->chunk_lts)) return US_ERR_ARG;
         stg = opts->variant;
+        ch_only = opts->chunk_lts;
         const int s = opts->split_k;
         if (s != 0) {
             if (s != 1 && s != 2 && s != 4 && s != 8 && s != 16) return US_ERR_ARG;
@@ -101,7 +105,7 @@ extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t bits,
         }
     }
     int wpg = 0, cfg = -1;
-    choose_config(M, K, std::min(N, US_N_MAX), reordered != 0, bits, device_cus(), wpg_only, stg, wpg, cfg);
+    choose_config(M, K, std::min(N, US_N_MAX), reordered != 0, bits, device_cus(), wpg_only, stg, ch_only, wpg, cfg);
     if (cfg < 0) return US_ERR_ARG;
     *split_k = wpg;
     *chunk_lts = kCfgs[cfg].ch;
@@ -114,7 +118,8 @@ extern "C" us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, con
     if (!bytes) return US_ERR_ARG;
     if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
     if (N < 1 || N > US_N_LIMIT) return US_ERR_SHAPE;
-    if (opts && (opts->variant < 0 || opts->variant > 2 || opts->split_k < 0)) return US_ERR_ARG;
+    if (opts && (opts->variant < 0 || opts->variant > 2 || opts->split_k < 0 || !chunk_option_ok(opts->chunk_lts)))
+        return US_ERR_ARG;
     *bytes = 0;
     return US_OK;
 }
@@ -142,10 +147,12 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     if (bits != 4 && bits != 2) return US_ERR_FORMAT;
     if (bits == 2 && perm) return US_ERR_ARG;              // no reordered 2-bit kernels
 
-    int wpg_only = 0, staging = 0;
+    int wpg_only = 0, staging = 0, ch_only = 0;
     if (opts) {
         if (opts->variant < 0 || opts->variant > 2) return US_ERR_ARG;
+        if (!chunk_option_ok(opts->chunk_lts)) return US_ERR_ARG;
         staging = opts->variant;
+        ch_only = opts->chunk_lts;
         const int s = opts->split_k;
         if (s != 0) {
             if (s != 1 && s != 2 && s != 4 && s != 8 && s != 16) return US_ERR_ARG;
@@ -159,8 +166,8 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     const int n_cu = device_cus();
     const int n_full = std::min<int>(N, US_N_MAX), n_last = N % US_N_MAX == 0 ? n_full : N % US_N_MAX;
     int wpg = 0, cfg = -1, wpg_last = 0, cfg_last = -1;
-    choose_config(M, K, n_full, perm, bits, n_cu, wpg_only, staging, wpg, cfg);
-    choose_config(M, K, n_last, perm, bits, n_cu, wpg_only, staging, wpg_last, cfg_last);
+    choose_config(M, K, n_full, perm, bits, n_cu, wpg_only, staging, ch_only, wpg, cfg);
+    choose_config(M, K, n_last, perm, bits, n_cu, wpg_only, staging, ch_only, wpg_last, cfg_last);
     if (cfg < 0 || cfg_last < 0) return US_ERR_ARG;        // no configuration fits LDS
 
     SpmmArgs a;

@@ -247,7 +247,8 @@ def test_pack_int4_layout():
     (4096, 11008, 8, (16, 11, 1)),     # one generation of 16-wavefront workgroups
     (12288, 4096, 8, (4, 16, 2)),      # the ring lets three workgroups share a CU
     (28672, 8192, 1, (2, 16, 1)),      # four chunks per slice, one generation
-    (28672, 8192, 32, (2, 4, 1)),      # two column blocks: at most 4 slices
+    (28672, 8192, 32, (2, 4, 1)),      # two column blocks, 1792 row blocks: two generations would cost more
+    (4096, 11008, 32, (16, 4, 1)),     # 256 row blocks: one generation, so 16 slices of three 4-LT chunks
 ])
 def test_plan_choices(M, K, N, plan):
     assert binding.spmm_plan(M, K, N) == plan
