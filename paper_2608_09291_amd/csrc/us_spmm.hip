@@ -194,6 +194,7 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
         a.N = ns;
         const hipError_t err = bits == 2 ? launch_cfg_w2(sw, sc, a, s)
                                : perm    ? launch_cfg_perm(sw, sc, a, s)
+                               : ns <= 4 ? launch_cfg_narrow(sw, sc, a, s)
                                          : launch_cfg<false, 4>(sw, sc, a, s);
         if (err != hipSuccess) return US_ERR_DEVICE;
     }

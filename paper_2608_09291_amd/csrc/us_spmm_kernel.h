@@ -1,6 +1,7 @@
 // IE-BME x INT4 -> INT32 sparse product on gfx950 (CDNA4): the kernel and
-// its launch templates, shared by us_spmm.hip (rows in stored order) and
-// us_spmm_perm.hip (row-reordered LTs).
+// its launch templates, shared by us_spmm.hip (4-bit weights, rows in stored
+// order), us_spmm_perm.hip (row-reordered LTs) and us_spmm_w2.hip (2-bit
+// weights).
 //
 // The operation is the UnionSparse kernel of Section VI: Y = W X with W in
 // IE-BME (Section V-A), X dense INT4, INT32 accumulation. What is kept from
@@ -36,8 +37,8 @@
 //    chunk by a DPP scan over 16 lanes and kept in LDS as a stage bit address;
 //    each lane adds the popcount of its row below bit 8 g. The same index then
 //    reads area stream q = 2a (columns 8g..8g+7) and stream q = 2a + 1
-//    (columns 32+8g..32+8g+7), the paper's "one rank reused across all area
-//    streams". Active nibbles are placed into their byte slots with two
+//    (columns 32+8g..32+8g+7): as in the paper, one rank serves every area
+//    stream. Active nibbles are placed into their byte slots with two
 //    v_perm_b32 per 8 positions, selectors taken from a 256-entry table
 //    indexed by the 8-bit segment; inactive slots get selector 0x0C (zero).
 //    LTs are decoded in pairs so that two independent chains interleave.
@@ -128,7 +129,8 @@ __device__ inline u32x2 perm_selectors(uint32_t m) {
 //   bases   : per LT and lane row rr = 2i + a, the LDS bit address of the
 //             first value of row i in area stream 2a (folded into the ring
 //             with RING; 16 dwords per LT);
-//   sd      : per LT, the number of bits of one area stream (o_{t+1} - o_t);
+//   sd      : per LT, the number of bits of one area stream,
+//             BITS (o_{t+1} - o_t) / 4;
 //   offsets : o_t of the chunk's LTs and the end offset (CH + 1 dwords);
 //   perm    : (PERM only) the row permutation word of each LT, 8 bytes;
 //   rows    : (PERM only) per LT and lane row, the union-mask row that lane
@@ -175,11 +177,6 @@ struct SpmmArgs {
 __device__ __forceinline__ uint32_t lds_load(uint32_t addr) { return *(const lds_u32 *)(size_t)addr; }
 // Two consecutive dwords at a 4-byte aligned address.
 __device__ __forceinline__ uint2 lds_load2(uint32_t addr) { return make_uint2(lds_load(addr), lds_load(addr + 4)); }
-// An 8-byte aligned pair.
-__device__ __forceinline__ uint2 lds_load_u2(uint32_t addr) {
-    const u32x2 v = *(const lds_u2 *)(size_t)addr;
-    return make_uint2(v.x, v.y);
-}
 __device__ __forceinline__ void lds_store(uint32_t addr, uint32_t v) { *(lds_u32 *)(size_t)addr = v; }
 __device__ __forceinline__ void lds_store2(uint32_t addr, u32x2 v) { *(lds_u2 *)(size_t)addr = v; }
 __device__ __forceinline__ void lds_store4(uint32_t addr, u32x4 v) { *(lds_u4 *)(size_t)addr = v; }
@@ -212,7 +209,8 @@ __device__ __forceinline__ uint32_t lane_value(uint32_t v, int lane) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
 
-// 32 bits of LDS starting at LDS bit address bn (nibble index * 4).
+// 32 bits of LDS starting at LDS bit address bn (payload value index * BITS,
+// relative to the stage).
 __device__ __forceinline__ uint32_t window(uint32_t bn) {
     const uint2 d = lds_load2((bn >> 3) & ~3u);
     return __builtin_amdgcn_alignbit(d.y, d.x, bn);
@@ -276,12 +274,17 @@ __device__ __forceinline__ i32x4 unpack_x(uint2 x) {
 // one chunk ahead); otherwise every slice is a single chunk. RING: the
 // payload is staged in a 4 KB ring instead of whole (see Chunk). PERM: the
 // LTs were row-reordered and p.perm32 holds their permutations. BITS: bits
-// per payload value (4, or 2 for W2A4). The host's
-// configuration choice assumes four resident wavefronts per SIMD, i.e. at
-// most 128 VGPRs: PERM variants are held to that explicitly (their
-// multi-chunk forms would take up to 144), the others stay under it.
-template <int WPG, int NB, int CH, bool MULTI, bool RING, bool PERM, int BITS>
-__global__ __launch_bounds__(64 * WPG, PERM ? 4 : 1) void us_spmm_kernel(SpmmArgs p, int stage_bytes) {
+// per payload value (4, or 2 for W2A4). NMAX: the widest activation matrix
+// the instantiation stages (4, 16 or 32; NB = 2 column blocks above 16): the
+// activation-staging registers are sized for it, so the N <= 4 kernels of
+// the decode regime keep about 30 fewer VGPRs live and are held to five
+// wavefronts per SIMD. The host's configuration choice assumes at least
+// four resident wavefronts per SIMD, i.e. at most 128 VGPRs: PERM variants
+// are held to that explicitly (their multi-chunk forms would take up to
+// 144), the others stay under it.
+template <int WPG, int NMAX, int CH, bool MULTI, bool RING, bool PERM, int BITS>
+__global__ __launch_bounds__(64 * WPG, NMAX <= 4 ? 5 : PERM ? 4 : 1) void us_spmm_kernel(SpmmArgs p, int stage_bytes) {
+    constexpr int NB = NMAX > 16 ? 2 : 1;                 // MFMA column blocks
     using C = Chunk<CH, RING, PERM, BITS>;
     static_assert(BITS == 4 || BITS == 2, "payload values are 4 or 2 bits");
     constexpr int kValShift = BITS == 4 ? 1 : 2;          // log2(values per byte)
@@ -330,7 +333,7 @@ __global__ __launch_bounds__(64 * WPG, PERM ? 4 : 1) void us_spmm_kernel(SpmmArg
     // q = lane + 64 u is row q / (2 CH), piece q % (2 CH). Only the loads
     // that carry pieces are issued: the texture path, not HBM, limits how
     // fast a CU takes them in at the start of the kernel.
-    constexpr int kXLoads = (16 * NB * C::kXPieces + 63) / 64;
+    constexpr int kXLoads = (NMAX * C::kXPieces + 63) / 64;
     const int x_loads = (N * C::kXPieces + 63) / 64;                           // wave-uniform
     uint32_t xv[kXLoads], xs[kXLoads];                     // global byte offset, LDS address
 #pragma unroll
@@ -627,16 +630,16 @@ inline int lds_bytes(int idx, int N, int wpg, bool perm, int bits) {
     return perm ? lds_bytes_t<true, 4>(idx, N, wpg) : lds_bytes_t<false, 4>(idx, N, wpg);
 }
 
-template <int WPG, int NB, int CH, bool RING, bool PERM, int BITS>
+template <int WPG, int NMAX, int CH, bool RING, bool PERM, int BITS>
 hipError_t launch_spmm(const SpmmArgs &a, hipStream_t s) {
     const bool multi = (a.nkb + WPG - 1) / WPG > CH;
-    auto kern = multi ? us_spmm_kernel<WPG, NB, CH, true, RING, PERM, BITS>
-                      : us_spmm_kernel<WPG, NB, CH, false, RING, PERM, BITS>;
+    auto kern = multi ? us_spmm_kernel<WPG, NMAX, CH, true, RING, PERM, BITS>
+                      : us_spmm_kernel<WPG, NMAX, CH, false, RING, PERM, BITS>;
     // Allow more than 64 KB of dynamic LDS (set once per instantiation).
     static const hipError_t attr =
-        (hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, true, RING, PERM, BITS>,
+        (hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NMAX, CH, true, RING, PERM, BITS>,
                              hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes),
-         hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NB, CH, false, RING, PERM, BITS>,
+         hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NMAX, CH, false, RING, PERM, BITS>,
                              hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes));
     (void)attr;
     const int st = stage_bytes<CH, RING, PERM, BITS>(a.N);
@@ -644,37 +647,41 @@ hipError_t launch_spmm(const SpmmArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <int NB, int CH, bool RING, bool PERM, int BITS>
+template <int NMAX, int CH, bool RING, bool PERM, int BITS>
 hipError_t launch_spmm_wpg(int wpg, const SpmmArgs &a, hipStream_t s) {
     switch (wpg) {
-        case 1: return launch_spmm<1, NB, CH, RING, PERM, BITS>(a, s);
-        case 2: return launch_spmm<2, NB, CH, RING, PERM, BITS>(a, s);
-        case 4: return launch_spmm<4, NB, CH, RING, PERM, BITS>(a, s);
-        case 8: return launch_spmm<8, NB, CH, RING, PERM, BITS>(a, s);
-        default: return launch_spmm<16, NB, CH, RING, PERM, BITS>(a, s);
+        case 1: return launch_spmm<1, NMAX, CH, RING, PERM, BITS>(a, s);
+        case 2: return launch_spmm<2, NMAX, CH, RING, PERM, BITS>(a, s);
+        case 4: return launch_spmm<4, NMAX, CH, RING, PERM, BITS>(a, s);
+        case 8: return launch_spmm<8, NMAX, CH, RING, PERM, BITS>(a, s);
+        default: return launch_spmm<16, NMAX, CH, RING, PERM, BITS>(a, s);
     }
 }
 
-// Launch configuration idx of kCfgs with wpg wavefronts per workgroup.
-template <bool PERM, int BITS>
+// Launch configuration idx of kCfgs with wpg wavefronts per workgroup, for
+// N <= 16 (NMAX = 4 or 16) or N <= 32.
+template <bool PERM, int BITS, int NMAX = 16>
 hipError_t launch_cfg(int wpg, int idx, const SpmmArgs &a, hipStream_t s) {
-    if (a.N > 16)
-        return idx == 1 ? launch_spmm_wpg<2, 8, false, PERM, BITS>(wpg, a, s)
-                        : launch_spmm_wpg<2, 4, false, PERM, BITS>(wpg, a, s);
+    if constexpr (NMAX > 4) {
+        if (a.N > 16)
+            return idx == 1 ? launch_spmm_wpg<32, 8, false, PERM, BITS>(wpg, a, s)
+                            : launch_spmm_wpg<32, 4, false, PERM, BITS>(wpg, a, s);
+    }
     switch (idx) {
-        case 5: return launch_spmm_wpg<1, 11, true, PERM, BITS>(wpg, a, s);
-        case 4: return launch_spmm_wpg<1, 16, true, PERM, BITS>(wpg, a, s);
-        case 3: return launch_spmm_wpg<1, 16, false, PERM, BITS>(wpg, a, s);
-        case 2: return launch_spmm_wpg<1, 11, false, PERM, BITS>(wpg, a, s);
-        case 1: return launch_spmm_wpg<1, 8, false, PERM, BITS>(wpg, a, s);
-        default: return launch_spmm_wpg<1, 4, false, PERM, BITS>(wpg, a, s);
+        case 5: return launch_spmm_wpg<NMAX, 11, true, PERM, BITS>(wpg, a, s);
+        case 4: return launch_spmm_wpg<NMAX, 16, true, PERM, BITS>(wpg, a, s);
+        case 3: return launch_spmm_wpg<NMAX, 16, false, PERM, BITS>(wpg, a, s);
+        case 2: return launch_spmm_wpg<NMAX, 11, false, PERM, BITS>(wpg, a, s);
+        case 1: return launch_spmm_wpg<NMAX, 8, false, PERM, BITS>(wpg, a, s);
+        default: return launch_spmm_wpg<NMAX, 4, false, PERM, BITS>(wpg, a, s);
     }
 }
 
-// The row-reordered (4-bit) and the 2-bit instantiations live in their own
-// translation units.
+// The row-reordered (4-bit), the 2-bit and the narrow (N <= 4, 4-bit, rows
+// in stored order) instantiations live in their own translation units.
 hipError_t launch_cfg_perm(int wpg, int idx, const SpmmArgs &a, hipStream_t s);
 hipError_t launch_cfg_w2(int wpg, int idx, const SpmmArgs &a, hipStream_t s);
+hipError_t launch_cfg_narrow(int wpg, int idx, const SpmmArgs &a, hipStream_t s);
 
 }  // namespace us_spmm_detail
 
