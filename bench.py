@@ -38,7 +38,8 @@ HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 1 << 30
 ROUND_LAUNCHES = 200
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_09291_amd", "csrc", f)
-               for f in ("us_spmm_kernel.h", "us_spmm.hip", "us_spmm_perm.hip")]
+               for f in ("us_spmm_kernel.h", "us_spmm.hip", "us_spmm_narrow.hip", "us_spmm_perm.hip",
+                         "us_spmm_w2.hip")]
 
 # HBM traffic of one SpMM launch, read from rocprofv3 --pmc runs of this
 # script (one pass for FETCH_SIZE, one for WRITE_SIZE; KiB per dispatch), each
@@ -50,7 +51,7 @@ KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_09291_amd", "csrc", f)
 # row reordering.
 COPY_FACTOR = {"FETCH_SIZE": 0.5, "WRITE_SIZE": 1.0}
 MEASURED_TRAFFIC = {
-    ("ffn_down_4096x11008_s50", 8, False): dict(src="48c7adef2f7aa178", FETCH_SIZE=11375.3, WRITE_SIZE=256.0),
+    ("ffn_down_4096x11008_s50", 8, False): dict(src="b7ef549b1dc1ea53", FETCH_SIZE=11374.8, WRITE_SIZE=256.0),
 }
 
 
