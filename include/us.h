@@ -14,7 +14,8 @@
  *   - a stream argument is a hipStream_t passed as void * (NULL = the null
  *     stream); GPU calls are asynchronous on that stream, never synchronise
  *     and never allocate device memory;
- *   - the library keeps no global state and is thread-safe.
+ *   - the only state the library keeps is a per-device cache (the compute-unit
+ *     count, kernel attributes applied once); every call is thread-safe.
  */
 #ifndef UNIONSPARSE_US_H
 #define UNIONSPARSE_US_H

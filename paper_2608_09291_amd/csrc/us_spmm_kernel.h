@@ -65,6 +65,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "us.h"
@@ -635,13 +636,20 @@ hipError_t launch_spmm(const SpmmArgs &a, hipStream_t s) {
     const bool multi = (a.nkb + WPG - 1) / WPG > CH;
     auto kern = multi ? us_spmm_kernel<WPG, NMAX, CH, true, RING, PERM, BITS>
                       : us_spmm_kernel<WPG, NMAX, CH, false, RING, PERM, BITS>;
-    // Allow more than 64 KB of dynamic LDS (set once per instantiation).
-    static const hipError_t attr =
-        (hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NMAX, CH, true, RING, PERM, BITS>,
-                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes),
-         hipFuncSetAttribute((const void *)us_spmm_kernel<WPG, NMAX, CH, false, RING, PERM, BITS>,
-                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes));
-    (void)attr;
+    // Allow more than 64 KB of dynamic LDS: once per instantiation and device
+    // (concurrent first calls may both set it, which is harmless).
+    static std::atomic<unsigned long long> attr_set{0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+    const unsigned long long bit = 1ull << (dev & 63);
+    if (!(attr_set.load(std::memory_order_acquire) & bit)) {
+        for (const void *f : {(const void *)us_spmm_kernel<WPG, NMAX, CH, true, RING, PERM, BITS>,
+                              (const void *)us_spmm_kernel<WPG, NMAX, CH, false, RING, PERM, BITS>}) {
+            const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds - kLutBytes);
+            if (e != hipSuccess) return e;
+        }
+        attr_set.fetch_or(bit, std::memory_order_release);
+    }
     const int st = stage_bytes<CH, RING, PERM, BITS>(a.N);
     hipLaunchKernelGGL(kern, dim3(a.M / 16), dim3(64 * WPG), WPG * st, s, a, st);
     return hipGetLastError();
