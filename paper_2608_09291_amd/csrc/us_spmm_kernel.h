@@ -566,10 +566,20 @@ __global__ __launch_bounds__(64 * WPG, NMAX <= 4 ? 5 : PERM ? 4 : 1) void us_spm
     // wait above counts loads exactly; later chunks only occur for long slices.
     // Every slice holds at least one LT (the host never splits K into more
     // slices than LTs), so the first chunk needs no branch.
+    // Multi-chunk slices lower their issue priority as they progress: 3 for
+    // the first quarter of the slice, one step less per quarter after it.
+    // A SIMD's arbiter otherwise favours its oldest wavefronts, and with equal
+    // work per slice the youngest workgroups of a CU then finish well after
+    // the oldest, with few wavefronts left to hide latency at the end.
+    if constexpr (MULTI) __builtin_amdgcn_s_setprio(3);
     stage_chunk(0);
     decode_chunk(0);
     if constexpr (MULTI) {
         for (int c0 = CH; c0 < nlt; c0 += CH) {
+            const int quarter = 4 * c0 / nlt;              // wave-uniform
+            if (quarter == 1) __builtin_amdgcn_s_setprio(2);
+            else if (quarter == 2) __builtin_amdgcn_s_setprio(1);
+            else if (quarter >= 3) __builtin_amdgcn_s_setprio(0);
             stage_chunk(c0);
             decode_chunk(c0);
         }
