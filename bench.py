@@ -227,7 +227,7 @@ def cpu_baseline(w, W, Xt, enc_bytes_alg, budget_s=12.0, bits=4):
     t_dec = time.perf_counter() - t0
     times = []
     t_start = time.perf_counter()
-    while len(times) < 3 or (time.perf_counter() - t_start < budget_s and len(times) < 50):
+    while len(times) < 3 or (time.perf_counter() - t_start < budget_s and len(times) < 5000):
         t = time.perf_counter()
         product.matmul_c(dense, Xt)
         times.append(time.perf_counter() - t)
