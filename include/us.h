@@ -30,7 +30,7 @@ extern "C" {
 typedef enum {
     US_OK = 0,
     US_ERR_ARG = -1,     /* null pointer, bad option value, misaligned pointer */
-    US_ERR_SHAPE = -2,   /* M % 16, K % 64, N outside [1, 32], size limits */
+    US_ERR_SHAPE = -2,   /* M % 16, K % 64, N outside [1, US_N_LIMIT], size limits */
     US_ERR_RANGE = -3,   /* a weight outside the signed INT4 range [-8, 7] */
     US_ERR_NOMEM = -4,   /* host allocation failed (encoder only) */
     US_ERR_DEVICE = -5,  /* the HIP launch reported an error */
