@@ -183,6 +183,7 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     a.M = M;
     a.K = K;
     a.nkb = (int32_t)nkb;
+    a.n_cu = n_cu;
 
     hipStream_t s = (hipStream_t)stream;
     for (int n0 = 0; n0 < N; n0 += US_N_MAX) {

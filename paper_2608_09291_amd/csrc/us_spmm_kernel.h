@@ -173,6 +173,7 @@ struct SpmmArgs {
     float *yf;
     const uint32_t *perm32; // row permutation words as dword pairs (PERM kernels)
     int32_t M, K, N, nkb;
+    int32_t n_cu;           // compute units of the device (wavefront priorities)
 };
 
 __device__ __forceinline__ uint32_t lds_load(uint32_t addr) { return *(const lds_u32 *)(size_t)addr; }
@@ -548,6 +549,9 @@ __global__ __launch_bounds__(64 * WPG, NMAX <= 4 ? 5 : PERM ? 4 : 1) void us_spm
                 lds_store4(st + 1024 * u + 16 * lane, (u32x4)pf[u]);
             }
             __asm__ volatile("" ::: "memory");
+            if constexpr (!MULTI) {
+                if (2 * j >= cnt) __builtin_amdgcn_s_setprio(0);   // second half: back to age order
+            }
             if constexpr (u + 1 < C::kLoads) {
                 const int ready = __builtin_popcountll(__builtin_amdgcn_ballot_w64(lane < cnt && need <= (uint32_t)u));
                 for (; j + 1 < ready; j += 2) decode_two();
@@ -571,7 +575,22 @@ __global__ __launch_bounds__(64 * WPG, NMAX <= 4 ? 5 : PERM ? 4 : 1) void us_spm
     // A SIMD's arbiter otherwise favours its oldest wavefronts, and with equal
     // work per slice the youngest workgroups of a CU then finish well after
     // the oldest, with few wavefronts left to hide latency at the end.
-    if constexpr (MULTI) __builtin_amdgcn_s_setprio(3);
+    //
+    // Single-chunk slices instead start at a priority that grows with their
+    // expected age rank on the CU: the workgroup's dispatch round (blockIdx /
+    // CUs) plus the wavefront's place among the workgroup's wavefronts on its
+    // SIMD (wave / 4), at most 3. Every wavefront returns to 0 once half of
+    // its slice is decoded. The youngest wavefronts, which the arbiter
+    // would serve last, get ahead early and the oldest catch up later, so
+    // that fewer wavefronts are left running alone at the end.
+    if constexpr (MULTI) {
+        __builtin_amdgcn_s_setprio(3);
+    } else {
+        const int rank = min(3, (int)blockIdx.x / max(p.n_cu, 1) + (wave >> 2));   // wave-uniform
+        if (rank == 1) __builtin_amdgcn_s_setprio(1);
+        else if (rank == 2) __builtin_amdgcn_s_setprio(2);
+        else if (rank >= 3) __builtin_amdgcn_s_setprio(3);
+    }
     stage_chunk(0);
     decode_chunk(0);
     if constexpr (MULTI) {
