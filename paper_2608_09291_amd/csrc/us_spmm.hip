@@ -19,26 +19,34 @@ bool aligned(const void *ptr, uintptr_t n) { return ((uintptr_t)ptr % n) == 0; }
 bool chunk_option_ok(int ch) { return ch == 0 || ch == 4 || ch == 8 || ch == 11 || ch == 16; }
 
 // Wavefronts per workgroup (= K slices per row block) and chunk
-// configuration. A wavefront pays one memory round trip (offsets, then
-// payload) per chunk, and a CU runs one generation of resident workgroups
-// after another; a generation also pays a cold start (kernel arguments,
-// selector table, first requests) worth about two chunk round trips. The
-// choice minimises generations x (2 + chunks per slice); ties go to fewer
-// generations, then to more wavefronts per CU, then to linear staging and
-// shorter chunks. (Fitted to a sweep of every configuration over 16 shapes
-// and widths: within 1 % of the fastest on average, 7 % at worst.) Residency: LDS, and at most 16 wavefronts per CU (the kernel's
-// registers). wpg_only > 0 fixes the number of wavefronts; staging 1 or 2
-// allows linear or ring payload staging only (0: either). perm: the LTs are
-// row-reordered (their stages hold two more per-LT arrays); bits: payload
-// value width (2-bit chunks stage half the payload bytes); ch_only > 0 fixes
-// the chunk length.
+// configuration, by a cost model of the kernel's time per CU, summed over
+// the generations of resident workgroups that a CU runs one after another:
+//   generation cost = 40 + chunks per slice * (20 + LTs per chunk * max(4, v)),
+// in quarters of one LT's decode time, with v the wavefronts on the busiest
+// CU in that generation. A generation pays a cold start (kernel arguments,
+// selector table, first requests) worth two chunk round trips; each chunk
+// pays one dependent memory round trip (offsets, then payload) worth five
+// LT decodes; and each LT's decode time grows with the wavefronts sharing a
+// SIMD (v / 4) once there is one per SIMD, as the decode is issue-bound.
+// Ties go to fewer generations, then to more wavefronts per CU, then to
+// linear staging and shorter chunks. The constants were fitted to a sweep of
+// every configuration over 17 shapes and widths: within 0.5 % of the fastest
+// on average, 4 % at worst. Residency: the LDS, and the wavefronts per SIMD
+// each instantiation is built for (waves_per_simd), with at most 16
+// workgroups per CU.
+// wpg_only > 0 fixes the number of wavefronts; staging 1 or 2 allows linear
+// or ring payload staging only (0: either). perm: the LTs are row-reordered
+// (their stages hold two more per-LT arrays); bits: payload value width
+// (2-bit chunks stage half the payload bytes); ch_only > 0 fixes the chunk
+// length.
 void choose_config(int M, int K, int N, bool perm, int bits, int n_cu, int wpg_only, int staging, int ch_only,
                    int &wpg, int &cfg) {
     const int nrb = M / 16, nkb = K / 64;
     long best[5] = {0, 0, 0, 0, 0};
     wpg = 0;
     cfg = -1;
-    constexpr long kGenCost = 2;                       // cold start of a generation, in chunk round trips
+    // Activation width the instantiation is built for (us_spmm's dispatch).
+    const int nmax = N > 16 ? 32 : (N <= 4 && bits == 4 && !perm) ? 4 : 16;
     for (int w = 16; w >= 1; w /= 2) {
         if (w > nkb || (wpg_only > 0 && w != wpg_only)) continue;
         for (int idx = 0; idx < kNumCfgs; ++idx) {
@@ -48,11 +56,18 @@ void choose_config(int M, int K, int N, bool perm, int bits, int n_cu, int wpg_o
             const int lds = lds_bytes(idx, N, w, perm, bits);
             if (lds > kMaxLds) continue;
             const int c = kCfgs[idx].ch;
-            const int per_cu = max(1, min(kMaxLds / lds, 16 / w));      // resident workgroups per CU
-            const long gens = (nrb + (long)n_cu * per_cu - 1) / ((long)n_cu * per_cu);
             const long chunks = ((nkb + w - 1) / w + c - 1) / c;
+            const int by_regs = 4 * waves_per_simd(w, nmax, c, chunks > 1, kCfgs[idx].ring, perm) / w;
+            const int per_cu = max(1, min(min(kMaxLds / lds, by_regs), 16));   // resident workgroups per CU
+            const long slots = (long)n_cu * per_cu;
+            const long gens = (nrb + slots - 1) / slots;
             const long waves = (long)w * min((long)per_cu, (nrb + n_cu - 1) / (long)n_cu);
-            const long key[5] = {gens * (kGenCost + chunks), gens, -waves, kCfgs[idx].ring ? 1 : 0, c};
+            long cost = 0;
+            for (long left = nrb; left > 0; left -= slots) {
+                const long v = (long)w * ((min(left, slots) + n_cu - 1) / n_cu);   // busiest CU
+                cost += 40 + chunks * (20 + c * max(4L, v));
+            }
+            const long key[5] = {cost, gens, -waves, kCfgs[idx].ring ? 1 : 0, c};
             bool better = cfg < 0;
             for (int k = 0; k < 5 && !better; ++k) {
                 if (key[k] != best[k]) {

@@ -20,11 +20,13 @@
 //    its payload with 16-byte buffer loads (a few in flight, the rest issued
 //    as earlier ones land) while the bitmaps and the activation slice, which
 //    were requested together with the offsets, are copied into the
-//    wavefront's own LDS stage. The payload is staged whole or through a
-//    4 KB ring (see Chunk); a slice of several chunks requests the next
-//    chunk's inputs ahead of the current payload. A wavefront's LDS accesses
-//    execute in order, so no workgroup barrier is needed between staging
-//    and decoding. The host picks the split, the chunk length and the
+//    wavefront's own LDS stage. The payload is staged whole (loaded straight
+//    into LDS up to 16 activation columns, via registers above) or through
+//    a 4 KB ring via registers (see Chunk); a slice of
+//    several chunks requests the next chunk's inputs ahead of the current
+//    payload. Only the wavefront itself reads its stage: its vmcnt waits and
+//    its in-order LDS accesses order staging before decoding, with no
+//    workgroup barrier. The host picks the split, the chunk length and the
 //    staging per shape (choose_config).
 //
 //  * Decode (the paper's LSPD, Section VI-B). One LT (16 x 64) is decoded by
@@ -176,6 +178,30 @@ struct SpmmArgs {
     int32_t n_cu;           // compute units of the device (wavefront priorities)
 };
 
+// Resident wavefronts per SIMD an instantiation is built for: its launch
+// bound, and the host's residency model. The figures sit at or above what
+// the kernels need: single-chunk slices keep only one chunk's state (at most
+// 64 VGPRs with four or more wavefronts per workgroup, 80 otherwise);
+// multi-chunk slices also hold the next chunk's inputs, more of them for
+// longer chunks and wider activation tiles, and ring staging, like every
+// kernel above 16 activation columns, holds the payload pieces in flight in
+// registers.
+constexpr int waves_per_simd(int wpg, int nmax, int ch, bool multi, bool ring, bool perm) {
+    return nmax > 16   ? (multi ? 4 : wpg >= 4 ? 7 : 6)
+           : !multi    ? (wpg >= 4 ? 8 : 6)
+           : ring      ? (nmax <= 4 ? 5 : 4)
+           : nmax <= 4 ? 7
+                       : (ch <= 4 ? 7 : ch <= 11 ? 5 : 4);
+}
+
+// The launch bound itself: waves_per_simd, except for the kernels above 16
+// activation columns on rows in stored order, which are left to the
+// compiler. Their natural use (at most 128 VGPRs, four wavefronts per
+// SIMD) is what waves_per_simd assumes, and a bound makes their code slower.
+constexpr int launch_waves(int wpg, int nmax, int ch, bool multi, bool ring, bool perm) {
+    return nmax > 16 && !perm ? 1 : waves_per_simd(wpg, nmax, ch, multi, ring, perm);
+}
+
 __device__ __forceinline__ uint32_t lds_load(uint32_t addr) { return *(const lds_u32 *)(size_t)addr; }
 // Two consecutive dwords at a 4-byte aligned address.
 __device__ __forceinline__ uint2 lds_load2(uint32_t addr) { return make_uint2(lds_load(addr), lds_load(addr + 4)); }
@@ -197,6 +223,21 @@ __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 __device__ __forceinline__ void wait_vm_all() { wait_vm<0>(); }
+
+// 16 bytes per lane from a raw buffer (descriptor `desc`, byte offset voff +
+// soff) straight into LDS: lane l writes LDS bytes [lds + 16 l, lds + 16 l +
+// 16) (buffer_load_dwordx4 with the LDS bit; M0 holds the LDS base, and one
+// wait state separates its write from the load). The load is counted by
+// vmcnt like any other, and the callers order their LDS reads after it with
+// their own vmcnt waits. It is issued from assembly because the compiler,
+// unable to tell which later LDS reads it may alias, would otherwise wait
+// for it before every one of them.
+__device__ __forceinline__ void dma16(u32x4 desc, uint32_t lds, uint32_t voff, uint32_t soff) {
+    __asm__ volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen nt lds"
+                     :
+                     : "s"(lds), "v"(voff), "s"(desc), "s"(soff)
+                     : "memory", "m0");
+}
 
 // f(std::integral_constant<int, U>) for U = B .. E-1, as straight-line code.
 template <int B, int E, typename F>
@@ -279,13 +320,13 @@ __device__ __forceinline__ i32x4 unpack_x(uint2 x) {
 // per payload value (4, or 2 for W2A4). NMAX: the widest activation matrix
 // the instantiation stages (4, 16 or 32; NB = 2 column blocks above 16): the
 // activation-staging registers are sized for it, so the N <= 4 kernels of
-// the decode regime keep about 30 fewer VGPRs live and are held to five
-// wavefronts per SIMD. The host's configuration choice assumes at least
-// four resident wavefronts per SIMD, i.e. at most 128 VGPRs: PERM variants
-// are held to that explicitly (their multi-chunk forms would take up to
-// 144), the others stay under it.
+// the decode regime keep about 30 fewer VGPRs live. Every instantiation is
+// built for waves_per_simd() resident wavefronts per SIMD (at most
+// 512 / that many VGPRs), which is also what the host's residency model
+// assumes.
 template <int WPG, int NMAX, int CH, bool MULTI, bool RING, bool PERM, int BITS>
-__global__ __launch_bounds__(64 * WPG, NMAX <= 4 ? 5 : PERM ? 4 : 1) void us_spmm_kernel(SpmmArgs p, int stage_bytes) {
+__global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, PERM)) void us_spmm_kernel(
+    SpmmArgs p, int stage_bytes) {
     constexpr int NB = NMAX > 16 ? 2 : 1;                 // MFMA column blocks
     using C = Chunk<CH, RING, PERM, BITS>;
     static_assert(BITS == 4 || BITS == 2, "payload values are 4 or 2 bits");
@@ -381,10 +422,23 @@ __global__ __launch_bounds__(64 * WPG, NMAX <= 4 ? 5 : PERM ? 4 : 1) void us_spm
     // Chunk state shared by the staging and the decoding half.
     int cnt = 0;
     uint32_t A0 = 0;
-    __amdgpu_buffer_rsrc_t psrc;
+    __amdgpu_buffer_rsrc_t psrc;                          // payload, through registers
+    u32x4 pdesc;                                          // the same range as a plain descriptor
     i32x4 pf[C::kLoads];
+    // Payload piece u (16 bytes per lane from the chunk's first staged byte
+    // on, stage bytes [1024 u, 1024 u + 1024)). Ring staging goes through
+    // registers, as its slots are refilled. Whole staging up to 16
+    // activation columns loads straight into the stage, which keeps the
+    // pieces out of the registers (measured slower above 16 columns); its
+    // last load writes only the pieces the payload area holds.
     auto load_piece = [&](int u) {
         pf[u] = __builtin_amdgcn_raw_buffer_load_b128(psrc, (uint32_t)(16 * lane + 1024 * u), 0, kNonTemporal);
+    };
+    constexpr bool kDirect = !RING && NMAX <= 16;         // payload straight into LDS
+    auto dma_piece = [&](auto uc) {
+        constexpr int u = decltype(uc)::value;
+        if (u + 1 < C::kLoads || C::kPayPieces % 64 == 0 || lane + 64 * u < C::kPayPieces)
+            dma16(pdesc, st + 1024u * u, (uint32_t)(16 * lane), 1024u * u);
     };
 
     auto stage_chunk = [&](int c0) {
@@ -402,11 +456,19 @@ __global__ __launch_bounds__(64 * WPG, NMAX <= 4 ? 5 : PERM ? 4 : 1) void us_spm
         // machine's requests and decoding starts while the rest streams.
         // Non-temporal: the stream does not displace the activations, which
         // every workgroup re-reads, from L2.
-        psrc = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)(p.pay + A0), (short)0, (int)min(16u * nq, (uint32_t)p.pay_bytes - A0), kBufferDword3);
+        const uint32_t prange = min(16u * nq, (uint32_t)p.pay_bytes - A0);
+        if constexpr (!kDirect) {
+            psrc = __builtin_amdgcn_make_buffer_rsrc((void *)(p.pay + A0), (short)0, (int)prange, kBufferDword3);
+        } else {
+            const uint64_t pa = (uint64_t)(size_t)(p.pay + A0);
+            pdesc = (u32x4){(uint32_t)pa, (uint32_t)(pa >> 32) & 0xFFFFu, prange, (uint32_t)kBufferDword3};
+        }
         auto issue_window = [&]() {
             static_for<0, kWindow>([&](auto uc) {
-                if constexpr (decltype(uc)::value < C::kLoads) load_piece(decltype(uc)::value);
+                if constexpr (decltype(uc)::value < C::kLoads) {
+                    if constexpr (!kDirect) load_piece(decltype(uc)::value);
+                    else dma_piece(uc);
+                }
             });
         };
         // Bitmaps (zero past the chunk), offsets and activations into the stage.
@@ -541,12 +603,16 @@ __global__ __launch_bounds__(64 * WPG, NMAX <= 4 ? 5 : PERM ? 4 : 1) void us_spm
             constexpr int u = decltype(uc)::value;
             constexpr int later = (kWindow - 1 < C::kLoads - 1 - u) ? kWindow - 1 : C::kLoads - 1 - u;
             wait_vm<later>();                              // piece u has landed
-            if constexpr (u + kWindow < C::kLoads) load_piece(u + kWindow);
-            if constexpr (RING) {
-                lds_store4(st + 1024 * (u & 3) + 16 * lane, (u32x4)pf[u]);
-                if ((u & 3) == 0 && lane < C::kGuard / 16) lds_store4(st + C::kRing + 16 * lane, (u32x4)pf[u]);
-            } else if (u + 1 < C::kLoads || lane + 64 * u < C::kPayPieces) {
-                lds_store4(st + 1024 * u + 16 * lane, (u32x4)pf[u]);
+            if constexpr (kDirect) {
+                if constexpr (u + kWindow < C::kLoads) dma_piece(std::integral_constant<int, u + kWindow>());
+            } else {
+                if constexpr (u + kWindow < C::kLoads) load_piece(u + kWindow);
+                if constexpr (RING) {
+                    lds_store4(st + 1024 * (u & 3) + 16 * lane, (u32x4)pf[u]);
+                    if ((u & 3) == 0 && lane < C::kGuard / 16) lds_store4(st + C::kRing + 16 * lane, (u32x4)pf[u]);
+                } else if (u + 1 < C::kLoads || lane + 64 * u < C::kPayPieces) {
+                    lds_store4(st + 1024 * u + 16 * lane, (u32x4)pf[u]);
+                }
             }
             __asm__ volatile("" ::: "memory");
             if constexpr (!MULTI) {
