@@ -341,10 +341,12 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     const int N = p.N;
 
     // This wavefront's K slice: LTs t0 .. t0 + nlt - 1 of row block mb
-    // (nlt >= 1 because WPG <= K / 64).
+    // (nlt >= 1 because WPG <= K / 64). When the LTs do not divide evenly,
+    // the first K/64 mod WPG wavefronts take one more; the last ones, which
+    // the SIMDs serve last, are the short slices.
     const int nkb = p.nkb;
-    const int kb0 = wave * nkb / WPG;
-    const int nlt = (wave + 1) * nkb / WPG - kb0;
+    const int kb0 = wave * (nkb / WPG) + min(wave, nkb % WPG);
+    const int nlt = nkb / WPG + (wave < nkb % WPG ? 1 : 0);
     const int64_t t0 = (int64_t)mb * nkb + kb0;
 
     // Lane roles in the decode.
