@@ -181,7 +181,8 @@ struct SpmmArgs {
 // Resident wavefronts per SIMD an instantiation is built for: its launch
 // bound, and the host's residency model. The figures sit at or above what
 // the kernels need: single-chunk slices keep only one chunk's state (at most
-// 64 VGPRs with four or more wavefronts per workgroup, 80 otherwise);
+// 64 VGPRs with four or more wavefronts per workgroup, 72 above 16
+// activation columns, 80 with fewer wavefronts);
 // multi-chunk slices also hold the next chunk's inputs, more of them for
 // longer chunks and wider activation tiles, and ring staging, like every
 // kernel above 16 activation columns, holds the payload pieces in flight in
@@ -320,10 +321,10 @@ __device__ __forceinline__ i32x4 unpack_x(uint2 x) {
 // per payload value (4, or 2 for W2A4). NMAX: the widest activation matrix
 // the instantiation stages (4, 16 or 32; NB = 2 column blocks above 16): the
 // activation-staging registers are sized for it, so the N <= 4 kernels of
-// the decode regime keep about 30 fewer VGPRs live. Every instantiation is
-// built for waves_per_simd() resident wavefronts per SIMD (at most
-// 512 / that many VGPRs), which is also what the host's residency model
-// assumes.
+// the decode regime keep about 30 fewer VGPRs live. Every instantiation fits
+// waves_per_simd() resident wavefronts per SIMD (at most 512 / that many
+// VGPRs; held there by its launch bound, see launch_waves), which is also
+// what the host's residency model assumes.
 template <int WPG, int NMAX, int CH, bool MULTI, bool RING, bool PERM, int BITS>
 __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, PERM)) void us_spmm_kernel(
     SpmmArgs p, int stage_bytes) {
