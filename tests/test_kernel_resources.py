@@ -56,6 +56,12 @@ def kernels():
 
     with cf.ThreadPoolExecutor(max_workers=4) as ex:
         texts = list(ex.map(compile_unit, UNITS))
+    m0_lines = []
+    for text in texts:
+        lines = [ln.strip() for ln in text.splitlines()]
+        for i, ln in enumerate(lines):
+            if "m0" in ln and not ln.startswith(";") and not ln.startswith("."):
+                m0_lines.append((ln, lines[i + 1] if i + 1 < len(lines) else "", lines[i + 2] if i + 2 < len(lines) else ""))
     found = []
     for text in texts:
         for m in re.finditer(r"\.amdhsa_kernel (\S+)(.*?)\.end_amdhsa_kernel", text, re.S):
@@ -67,19 +73,34 @@ def kernels():
             scratch = int(re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", m.group(2)).group(1))
             found.append(dict(wpg=wpg, nmax=nmax, ch=ch, multi=bool(multi), ring=bool(ring), perm=bool(perm),
                               bits=bits, vgpr=vgpr, scratch=scratch))
-    return found
+    return found, m0_lines
 
 
-def test_every_configuration_is_built(kernels):
+@pytest.fixture(scope="module")
+def kernel_list(kernels):
+    return kernels[0]
+
+
+def test_m0_is_only_the_direct_payload_loads(kernels):
+    # The direct payload load sets M0 in assembly and lists it as clobbered;
+    # that is only sound while the compiler itself keeps nothing in M0.
+    m0 = kernels[1]
+    assert m0, "no direct payload loads found"
+    for ln, nxt, nxt2 in m0:
+        assert ln.startswith("s_mov_b32 m0,"), ln
+        assert nxt == "s_nop 0" and nxt2.startswith("buffer_load_dwordx4") and nxt2.endswith(" lds"), (ln, nxt, nxt2)
+
+
+def test_every_configuration_is_built(kernel_list):
     # 5 WPG x (4 linear + 2 ring chunk lengths) x single/multi for the N <= 4
     # and N <= 16 tiers, 5 x 2 x 2 for N <= 32, per translation unit.
-    assert len(kernels) >= 4 * 5 * 2 * 2
-    assert {k["nmax"] for k in kernels} == {4, 16, 32}
+    assert len(kernel_list) >= 4 * 5 * 2 * 2
+    assert {k["nmax"] for k in kernel_list} == {4, 16, 32}
 
 
-def test_registers_fit_the_residency_the_host_assumes(kernels):
+def test_registers_fit_the_residency_the_host_assumes(kernel_list):
     over = []
-    for k in kernels:
+    for k in kernel_list:
         w = waves_per_simd(k["wpg"], k["nmax"], k["ch"], k["multi"], k["ring"], k["perm"])
         budget = (512 // w) // 8 * 8
         if k["vgpr"] > budget:
@@ -87,7 +108,7 @@ def test_registers_fit_the_residency_the_host_assumes(kernels):
     assert not over, over[:5]
 
 
-def test_no_scratch_except_the_known_case(kernels):
-    spills = [k for k in kernels if k["scratch"]
+def test_no_scratch_except_the_known_case(kernel_list):
+    spills = [k for k in kernel_list if k["scratch"]
               and (k["nmax"], k["ch"], k["multi"], k["ring"], k["perm"]) not in KNOWN_SPILLS]
     assert not spills, spills[:5]
