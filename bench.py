@@ -232,12 +232,26 @@ def cpu_baseline(w, W, Xt, enc_bytes_alg, budget_s=12.0, bits=4):
         product.matmul_c(dense, Xt)
         times.append(time.perf_counter() - t)
     med = float(np.median(times))
+    # The same product on one core: a few calls, at most about 3 s.
+    product.set_threads(1)
+    one = []
+    t_start = time.perf_counter()
+    try:
+        while len(one) < 1 or (time.perf_counter() - t_start < 3.0 and len(one) < 20):
+            t = time.perf_counter()
+            product.matmul_c(dense, Xt)
+            one.append(time.perf_counter() - t)
+    finally:
+        product.set_threads(threads)
+    med1 = float(np.median(one))
     return dict(value=round(enc_bytes_alg / med / 1e9, 4), unit="GB/s", cores=threads, kind="oracle",
                 sample=(f"whole {w.M}x{w.K} matrix, N={Xt.shape[0]}: oracle int64 masked dense product "
                         f"(oracle/matmul_i64.c, OpenMP) over the oracle-decoded weights, median of "
-                        f"{len(times)} calls = {med * 1e3:.1f} ms/call; oracle encode+decode (numpy) "
+                        f"{len(times)} calls = {med * 1e3:.1f} ms/call; on one core, median of {len(one)} "
+                        f"calls = {med1 * 1e3:.1f} ms/call; oracle encode+decode (numpy) "
                         f"{t_dec:.2f} s, not included"),
-                ms_per_call=round(med * 1e3, 3))
+                ms_per_call=round(med * 1e3, 3), single_core_ms_per_call=round(med1 * 1e3, 3),
+                single_core_value=round(enc_bytes_alg / med1 / 1e9, 4))
 
 
 def copy_probe(torch, args, timer):

@@ -39,3 +39,14 @@ int oracle_max_threads(void)
     return 1;
 #endif
 }
+
+/* Threads for later products (n >= 1); used to time the product on one core. */
+void oracle_set_threads(int n)
+{
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}

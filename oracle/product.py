@@ -44,12 +44,19 @@ def _load():
                                           ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
         lib.oracle_matmul_i64.restype = None
         lib.oracle_max_threads.restype = ctypes.c_int
+        lib.oracle_set_threads.argtypes = [ctypes.c_int]
+        lib.oracle_set_threads.restype = None
         _lib = lib
     return _lib
 
 
 def max_threads() -> int:
     return int(_load().oracle_max_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads the C product uses from now on (for timing it on one core)."""
+    _load().oracle_set_threads(int(n))
 
 
 def matmul_c(W: np.ndarray, Xt: np.ndarray) -> np.ndarray:
