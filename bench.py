@@ -190,15 +190,22 @@ def spmm_bench(torch, args, w, N, timer, reorder=False, bits=4):
 
 
 def read_ceiling(torch, nbytes, steps, timer):
-    """Streaming-read rate of HBM at the same byte count, same rotation."""
+    """Streaming-read time of HBM at the same byte count, same rotation: the
+    fastest of the read probe's launch shapes. Returns (ms per read, shape)."""
     nbytes = (nbytes + 15) // 16 * 16
     n_copies = max(2, -(-ROTATE_BYTES // nbytes))
     bufs = [torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(i % 251) for i in range(n_copies)]
     sink = torch.empty(binding.probe_read_sink_words(nbytes), dtype=torch.int32, device="cuda")
-    timer.run(lambda i: binding.probe_read(bufs[i % n_copies], nbytes, sink), min(steps, 200))
-    ms = timer.run(lambda i: binding.probe_read(bufs[i % n_copies], nbytes, sink), steps)
+    best = None
+    for shape in range(binding.PROBE_READ_SHAPES):
+        def launch(i, shape=shape):
+            binding.probe_read(bufs[i % n_copies], nbytes, sink, shape)
+        timer.run(launch, min(steps, 200))
+        ms = timer.run(launch, steps) / steps
+        if best is None or ms < best[0]:
+            best = (ms, shape)
     del bufs
-    return ms / steps
+    return best
 
 
 def dense_gemm(torch, w, N, steps, timer):
@@ -300,9 +307,11 @@ def main():
 
     extras = {}
     if not args.no_extras:
-        ceil_ms = read_ceiling(torch, r["alg_bytes"], min(args.steps, 1000), timer)
+        ceil_ms, ceil_shape = read_ceiling(torch, r["alg_bytes"], min(args.steps, 1000), timer)
         extras["read_ceiling_gbs"] = round(r["alg_bytes"] / (ceil_ms * 1e-3) / 1e9, 1)
         extras["read_ceiling_us"] = round(ceil_ms * 1e3, 3)
+        extras["read_ceiling_shape"] = ceil_shape
+        extras["kernel_of_read_ceiling"] = round(ceil_ms / ms_step, 3)
         g_ms, g_bytes = dense_gemm(torch, w, N, min(args.steps, 1000), timer)
         extras["dense_int8_gemm_us"] = round(g_ms * 1e3, 3)
         extras["dense_int8_gemm_gbs"] = round(g_bytes / (g_ms * 1e-3) / 1e9, 1)

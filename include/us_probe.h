@@ -24,10 +24,20 @@
 extern "C" {
 #endif
 
+/* Launch shapes of us_probe_read: 0 = 256 threads per workgroup, 4 loads
+ * issued together, 8 workgroups per compute unit; 1 = 512, 4, 1; 2 = 1024,
+ * 4, 8; 3 = 256, 8, 1. No one shape is fastest at every size, so the read
+ * ceiling at a byte count is the fastest of them. */
+#define US_PROBE_READ_SHAPES 4
+
 /* Read `bytes` (a multiple of 16) from `src` (16-byte aligned) once, with
- * 16-byte loads, and fold them into one uint32 per workgroup at sink[0..]
- * (sink holds us_probe_read_sink_words(bytes) words). */
-us_status us_probe_read(const void *src, size_t bytes, uint32_t *sink, void *stream);
+ * non-temporal 16-byte loads in launch shape `shape` (0 ..
+ * US_PROBE_READ_SHAPES - 1), and fold them by XOR into one uint32 per
+ * wavefront at sink[wavefront index]. sink holds
+ * us_probe_read_sink_words(bytes) words, enough for every shape; on a
+ * zeroed sink the XOR of all its words is the XOR of the data. US_ERR_ARG
+ * for a null pointer, bad size or alignment, or an unknown shape. */
+us_status us_probe_read(const void *src, size_t bytes, uint32_t *sink, int32_t shape, void *stream);
 size_t us_probe_read_sink_words(size_t bytes);
 
 /* dst[0 .. bytes) = src[0 .. bytes); both 16-byte aligned, bytes % 16 == 0. */

@@ -105,7 +105,7 @@ def lib():
         L.us_gemm_i8.argtypes = [vp, vp, i32, i32, i32, vp, vp]
         L.us_status_string.argtypes = [ctypes.c_int]
         L.us_status_string.restype = ctypes.c_char_p
-        L.us_probe_read.argtypes = [vp, sz, vp, vp]
+        L.us_probe_read.argtypes = [vp, sz, vp, ctypes.c_int32, vp]
         L.us_probe_read_sink_words.argtypes = [sz]
         L.us_probe_read_sink_words.restype = sz
         L.us_probe_copy.argtypes = [vp, vp, sz, vp]
@@ -300,8 +300,12 @@ def gemm_i8(w, x, M: int, K: int, N: int, y, stream=None) -> None:
                                           _stream_handle(stream)))
 
 
-def probe_read(src, nbytes: int, sink, stream=None) -> None:
-    _check("us_probe_read", lib().us_probe_read(src.data_ptr(), nbytes, sink.data_ptr(),
+PROBE_READ_SHAPES = 4      # US_PROBE_READ_SHAPES
+
+
+def probe_read(src, nbytes: int, sink, shape: int = 0, stream=None) -> None:
+    """us_probe_read: one streaming read of nbytes in launch shape `shape`."""
+    _check("us_probe_read", lib().us_probe_read(src.data_ptr(), nbytes, sink.data_ptr(), shape,
                                                 _stream_handle(stream)))
 
 

@@ -105,36 +105,57 @@ constexpr int kProbeThreads = 256;
 constexpr int kProbeUnroll = 4;
 constexpr size_t kProbeMaxBlocks = 4096;
 
+// Workgroups of the copy probe: one pass of kProbeUnroll pieces per thread,
+// at most kProbeMaxBlocks.
 size_t probe_blocks(size_t n16) {
     size_t b = (n16 + kProbeThreads * kProbeUnroll - 1) / (kProbeThreads * kProbeUnroll);
     if (b < 1) b = 1;
     return b < kProbeMaxBlocks ? b : kProbeMaxBlocks;
 }
 
-__global__ __launch_bounds__(kProbeThreads) void probe_read_kernel(const i32x4 *__restrict__ src, size_t n16,
-                                                                   uint32_t *__restrict__ sink) {
-    __shared__ uint32_t part[kProbeThreads];
+// Read probe shapes: threads per workgroup, 16-byte loads issued together
+// per thread, workgroups per compute unit. No one shape reads fastest at
+// every size on this GPU: many workgroups with few loads each win at tens of
+// MB, few large workgroups at hundreds of MB. A caller that wants the
+// ceiling times every shape and keeps the fastest.
+struct ProbeShape {
+    int threads, unroll, per_cu;
+};
+constexpr ProbeShape kReadShapes[US_PROBE_READ_SHAPES] = {{256, 4, 8}, {512, 4, 1}, {1024, 4, 8}, {256, 8, 1}};
+constexpr int kReadMaxWavesPerCu = 128;                 // 8 x 1024 / 64
+
+// Each thread reads pieces idx, idx + stride, ... (stride = all threads of
+// the grid), U at a time, and folds them into one word by XOR. The
+// wavefront folds its 64 words with lane shuffles, and lane 0 stores the
+// result at sink[wavefront index in the grid]: no barrier, and the XOR of
+// the words stored equals the XOR of the data read.
+template <int T, int U>
+__global__ __launch_bounds__(T) void probe_read_kernel(const i32x4 *__restrict__ src, size_t n16,
+                                                       uint32_t *__restrict__ sink) {
     uint32_t acc = 0;
-    const size_t stride = (size_t)gridDim.x * kProbeThreads;
-    size_t idx = (size_t)blockIdx.x * kProbeThreads + threadIdx.x;
-    for (; idx + (kProbeUnroll - 1) * stride < n16; idx += kProbeUnroll * stride) {
-        i32x4 v[kProbeUnroll];
+    const size_t stride = (size_t)gridDim.x * T;
+    size_t idx = (size_t)blockIdx.x * T + threadIdx.x;
+    for (; idx + (U - 1) * stride < n16; idx += U * stride) {
+        i32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < kProbeUnroll; ++u) v[u] = __builtin_nontemporal_load(src + idx + u * stride);
+        for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(src + idx + u * stride);
 #pragma unroll
-        for (int u = 0; u < kProbeUnroll; ++u) acc ^= (uint32_t)(v[u].x ^ v[u].y ^ v[u].z ^ v[u].w);
+        for (int u = 0; u < U; ++u) acc ^= (uint32_t)(v[u].x ^ v[u].y ^ v[u].z ^ v[u].w);
     }
     for (; idx < n16; idx += stride) {
         const i32x4 v = __builtin_nontemporal_load(src + idx);
         acc ^= (uint32_t)(v.x ^ v.y ^ v.z ^ v.w);
     }
-    part[threadIdx.x] = acc;
-    __syncthreads();
-    for (int h = kProbeThreads / 2; h > 0; h >>= 1) {
-        if ((int)threadIdx.x < h) part[threadIdx.x] ^= part[threadIdx.x + h];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) sink[blockIdx.x] = part[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o, 64);
+    if ((threadIdx.x & 63) == 0) sink[(size_t)blockIdx.x * (T / 64) + threadIdx.x / 64] = acc;
+}
+
+int probe_cus() {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 256;
+    return n;
 }
 
 __global__ __launch_bounds__(kProbeThreads) void probe_copy_kernel(const i32x4 *__restrict__ src,
@@ -176,13 +197,25 @@ extern "C" us_status us_gemm_i8(const int8_t *w, const int8_t *x, int32_t M, int
     return US_OK;
 }
 
-extern "C" size_t us_probe_read_sink_words(size_t bytes) { return probe_blocks(bytes / 16); }
+extern "C" size_t us_probe_read_sink_words(size_t bytes) {
+    (void)bytes;
+    return (size_t)kReadMaxWavesPerCu * (size_t)probe_cus();
+}
 
-extern "C" us_status us_probe_read(const void *src, size_t bytes, uint32_t *sink, void *stream) {
+extern "C" us_status us_probe_read(const void *src, size_t bytes, uint32_t *sink, int32_t shape, void *stream) {
     if (!src || !sink || bytes == 0 || bytes % 16 || !aligned16(src)) return US_ERR_ARG;
+    if (shape < 0 || shape >= US_PROBE_READ_SHAPES) return US_ERR_ARG;
     const size_t n16 = bytes / 16;
-    hipLaunchKernelGGL(probe_read_kernel, dim3((unsigned)probe_blocks(n16)), dim3(kProbeThreads), 0,
-                       (hipStream_t)stream, (const i32x4 *)src, n16, sink);
+    const ProbeShape sh = kReadShapes[shape];
+    const dim3 grid((unsigned)(sh.per_cu * probe_cus()));
+    const hipStream_t st = (hipStream_t)stream;
+    const i32x4 *s16 = (const i32x4 *)src;
+    switch (shape) {
+        case 0: hipLaunchKernelGGL((probe_read_kernel<256, 4>), grid, dim3(256), 0, st, s16, n16, sink); break;
+        case 1: hipLaunchKernelGGL((probe_read_kernel<512, 4>), grid, dim3(512), 0, st, s16, n16, sink); break;
+        case 2: hipLaunchKernelGGL((probe_read_kernel<1024, 4>), grid, dim3(1024), 0, st, s16, n16, sink); break;
+        default: hipLaunchKernelGGL((probe_read_kernel<256, 8>), grid, dim3(256), 0, st, s16, n16, sink); break;
+    }
     return hipGetLastError() == hipSuccess ? US_OK : US_ERR_DEVICE;
 }
 

@@ -230,8 +230,10 @@ def test_workspace_size_is_zero():
 
 def test_probe_argument_errors():
     L = binding.lib()
-    assert L.us_probe_read(None, 16, 0x10, None) == -1
-    assert L.us_probe_read(0x10, 15, 0x10, None) == -1
+    assert L.us_probe_read(None, 16, 0x10, 0, None) == -1
+    assert L.us_probe_read(0x10, 15, 0x10, 0, None) == -1
+    assert L.us_probe_read(0x10, 16, 0x10, -1, None) == -1
+    assert L.us_probe_read(0x10, 16, 0x10, binding.PROBE_READ_SHAPES, None) == -1
     assert L.us_probe_copy(0x10, 0x18, 16, None) == -1
     assert L.us_probe_spin(2 * 10 ** 9, None) == -1
 

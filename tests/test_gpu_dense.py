@@ -48,13 +48,15 @@ def test_probe_read_and_copy(torch_cuda):
     host = rng.integers(0, 256, size=n, dtype=np.uint8)
     src = torch.from_numpy(host).cuda()
     words = binding.probe_read_sink_words(n)
-    sink = torch.zeros(words, dtype=torch.int32, device="cuda")
-    binding.probe_read(src, n, sink)
+    expect = np.bitwise_xor.reduce(host.view(np.uint32))
+    for shape in range(binding.PROBE_READ_SHAPES):
+        sink = torch.zeros(words, dtype=torch.int32, device="cuda")
+        binding.probe_read(src, n, sink, shape)
+        torch.cuda.synchronize()
+        assert np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32)) == expect, shape
     dst = torch.zeros(n, dtype=torch.uint8, device="cuda")
     binding.probe_copy(src, dst, n)
     torch.cuda.synchronize()
-    folded = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
-    assert folded == np.bitwise_xor.reduce(host.view(np.uint32))
     assert np.array_equal(dst.cpu().numpy(), host)
 
 
