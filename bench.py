@@ -44,14 +44,15 @@ KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_09291_amd", "csrc", f)
 # HBM traffic of one SpMM launch, read from rocprofv3 --pmc runs of this
 # script (one pass for FETCH_SIZE, one for WRITE_SIZE; KiB per dispatch), each
 # divided by what the same counter reads per byte for the plain copy kernel
-# (bench.py --copy-probe 268435456: FETCH_SIZE reads 0.5 KiB and WRITE_SIZE
-# 1.0 KiB per KiB copied). An entry holds only for the kernel sources whose
+# (bench.py --copy-probe 268435456 copies 262144 KiB: FETCH_SIZE reads
+# 131082 KiB and WRITE_SIZE 262144 KiB per dispatch, i.e. 0.50004 and 1.0 KiB
+# per KiB copied). An entry holds only for the kernel sources whose
 # SHA-256 (of the files in KERNEL_SRCS, concatenated) starts with `src`;
 # after any change to them the traffic is unknown. Keyed by workload, N and
 # row reordering.
-COPY_FACTOR = {"FETCH_SIZE": 0.5, "WRITE_SIZE": 1.0}
+COPY_FACTOR = {"FETCH_SIZE": 131082.0 / 262144.0, "WRITE_SIZE": 262144.0 / 262144.0}
 MEASURED_TRAFFIC = {
-    ("ffn_down_4096x11008_s50", 8, False): dict(src="155a1b7dd80d4c75", FETCH_SIZE=11383.2, WRITE_SIZE=256.0),
+    ("ffn_down_4096x11008_s50", 8, False): dict(src="155a1b7dd80d4c75", FETCH_SIZE=11383.46875, WRITE_SIZE=256.0),
 }
 
 
