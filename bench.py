@@ -113,6 +113,7 @@ class Timer:
         total = 0.0
         done = 0
         retries = 0
+        self.batches = []                                  # (ms, launches) per timed batch
         while done < count:
             n = min(ROUND_LAUNCHES, count - done)
             spin_ns = int(max(2e6, n * per_launch_host_us * 1e3 * 2))
@@ -130,7 +131,9 @@ class Timer:
                 per_launch_host_us *= 4
                 retries += 1
                 continue
-            total += start.elapsed_time(end)
+            ms = start.elapsed_time(end)
+            self.batches.append((ms, n))
+            total += ms
             done += n
         return total
 
@@ -175,6 +178,7 @@ def spmm_bench(torch, args, w, N, timer, reorder=False, bits=4):
     timer.run(launch, args.warmup)
     torch.cuda.synchronize()
     ms = timer.run(launch, args.steps)
+    batches = [1e3 * b_ms / n for b_ms, n in timer.batches]   # µs per call, one value per timed batch
     if status[0]:
         raise binding.UsError("us_spmm", status[0])
 
@@ -187,7 +191,7 @@ def spmm_bench(torch, args, w, N, timer, reorder=False, bits=4):
     if w.dequant:
         alg += w.M * 4 + w.M * N * 4
     return dict(W=W, Xt=Xt, enc=enc, rep=rep, ms=ms, alg_bytes=alg, enc_bytes=enc_bytes,
-                n_copies=n_copies, y=y, yf=yf)
+                n_copies=n_copies, y=y, yf=yf, batches=batches)
 
 
 def read_ceiling(torch, nbytes, steps, timer):
@@ -347,6 +351,9 @@ def main():
                    "weights": f"w{args.bits}a4 IE-BME (16x64 tiles, 2x2 areas), int8 MFMA, int32 accumulate",
                    "rotating_copies": r["n_copies"]},
         "us_per_call": round(us, 3),
+        "us_per_call_batches": {"batches": len(r["batches"]), "max_launches_per_batch": ROUND_LAUNCHES,
+                                "median": round(float(np.median(r["batches"])), 3),
+                                "min": round(min(r["batches"]), 3), "max": round(max(r["batches"]), 3)},
         "dense_equiv_tops": round(tops, 2),
         "encoded_mb": round(r["alg_bytes"] / 1e6, 3),
         "pmr": round(rep["pmr"], 4),
