@@ -260,6 +260,9 @@ us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, const us_spmm_
  *   opts   : NULL for automatic choices
  *   stream : hipStream_t
  * Argument errors return before launch; a launch error returns US_ERR_DEVICE.
+ * The call never allocates, clears memory or synchronises, so it can be
+ * captured in a HIP graph. Call each shape once outside the capture first:
+ * the first call of a kernel configuration on a device sets its LDS limit.
  */
 us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N, int32_t *y,
                   const float *scale, float *y_f32, void *ws, size_t ws_bytes,
