@@ -217,6 +217,44 @@ def test_repeat_is_identical(torch_cuda):
     check(a[0], a[1], W, Xt, sc)
 
 
+def test_concurrent_threads_and_streams(torch_cuda):
+    # Two host threads, each with its own stream and matrix, call us_spmm at
+    # the same time (ctypes releases the interpreter lock during the call).
+    # Shapes not used elsewhere in this module, so that both threads may also
+    # take a configuration's first call together.
+    import threading
+    torch = torch_cuda
+    announce("two threads x 12 calls, M=176 K=2880 N=6 and M=208 K=1344 N=13")
+    cases = []
+    for seed, (M, K, N) in ((51, (176, 2880, 6)), (52, (208, 1344, 13))):
+        W, Xt, sc = synth.random_problem(M, K, N, 0.6, seed)
+        dev = binding.to_device(binding.encode(W))
+        xp = torch.from_numpy(binding.pack_int4(Xt)).cuda()
+        ys = [torch.full((N, M), SENTINEL, dtype=torch.int32, device="cuda") for _ in range(12)]
+        cases.append(dict(W=W, Xt=Xt, dev=dev, xp=xp, N=N, ys=ys, stream=torch.cuda.Stream(), err=[]))
+    torch.cuda.synchronize()
+
+    def work(c):
+        try:
+            with torch.cuda.stream(c["stream"]):
+                for y in c["ys"]:
+                    binding.spmm(c["dev"], c["xp"], c["N"], y, stream=c["stream"])
+            c["stream"].synchronize()
+        except Exception as e:          # reported by the main thread
+            c["err"].append(e)
+
+    threads = [threading.Thread(target=work, args=(c,)) for c in cases]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(60)
+    torch.cuda.synchronize()
+    for c in cases:
+        assert not c["err"], c["err"]
+        for y in c["ys"]:
+            check(y.cpu().numpy().T, None, c["W"], c["Xt"])
+
+
 def test_graph_capture_replays(torch_cuda):
     # us_spmm neither allocates, clears nor synchronises, so a HIP graph can
     # hold it. Two calls (two matrices, one with dequant) are captured once
