@@ -193,7 +193,14 @@ typedef struct {
  */
 us_status us_pmr_formats(const us_iebme *m, int32_t value_bits, int32_t N, us_format_report out[US_NUM_FORMATS]);
 
-/* An IE-BME matrix whose three arrays the caller has copied to the GPU. */
+/*
+ * An IE-BME matrix whose three arrays the caller has copied to the GPU
+ * (Section V-A, "IE-BME Storage Layout"). The arrays must be those an
+ * us_encode* call produced (bitmaps and offsets consistent, offsets
+ * non-decreasing and ending at n_payload); the GPU does not check them. For
+ * arrays that are not, Y is unspecified, but every payload read stays inside
+ * the payload array: the kernels clamp each slice's range to it.
+ */
 typedef struct {
     const uint64_t *bitmaps;      /* device, n_lt * 4 words, 8-byte aligned  */
     const uint32_t *offsets;      /* device, n_lt + 1 entries, 4-byte aligned */
@@ -207,33 +214,64 @@ typedef struct {
                                      cannot be row-reordered (US_ERR_ARG)  */
 } us_iebme_dev;
 
+/* Most K blocks a row block's K range can be split into across workgroups. */
+#define US_K_BLOCKS_MAX 64
+
+/*
+ * Launch options (all zero = automatic). The split-K of the paper's kernel
+ * (Section VI-C, "UnionSparse Kernel" algorithm: a grid of split-K batches by
+ * row tiles, each batch storing its partial tile to a reduction workspace,
+ * then a reduction) is realised at two levels: the wavefronts of a workgroup
+ * split one row block's K range and combine in LDS (split_k), and with
+ * k_blocks > 1 several workgroups split it and combine through the workspace.
+ */
 typedef struct {
-    int32_t split_k;  /* K slices per 16-row block, one wavefront each:
+    int32_t split_k;  /* K slices per workgroup, one wavefront each:
                          0 = automatic, else 1, 2, 4, 8 or 16; halved
-                         while it exceeds K / 64 (one LT per slice)      */
-    int32_t variant;  /* payload staging in LDS: 0 = automatic, 1 = whole
-                         chunk, 2 = 4 KB ring (N <= 16 only); a choice
-                         that fits no configuration returns US_ERR_ARG   */
+                         while it exceeds K / 64 (one LT per slice);
+                         required with variant 3                         */
+    int32_t variant;  /* payload staging: 0 = automatic, 1 = whole chunk,
+                         2 = 4 KB ring (N <= 16 only), 3 = single pass:
+                         each wavefront requests its whole slice at once
+                         (N <= 16 only); a choice that fits no
+                         configuration returns US_ERR_ARG                */
     int32_t chunk_lts; /* LTs per chunk: 0 = automatic, else 4, 8, 11 or
-                         16 (4 or 8 when N > 16); for tuning and tests   */
+                         16 (4 or 8 when N > 16); with variant 3 the most
+                         LTs per wavefront slice: 4, 8, 11, 16, 22 or 32;
+                         for tuning and tests                            */
+    int32_t k_blocks; /* workgroups per row block, each taking a
+                         contiguous K block: 0 or 1 = one (no workspace),
+                         2 .. US_K_BLOCKS_MAX with variant 3 only; needs
+                         the workspace (us_spmm_workspace_size)          */
 } us_spmm_opts;
 
 /*
  * us_spmm_plan - the launch configuration us_spmm would use for this shape
  * and options on the current device (a 256-CU MI355X when no device is
- * visible): K slices per 16-row block (one wavefront each), LTs per chunk,
- * and payload staging (1 whole chunk, 2 ring) of the first slab of
- * min(N, US_N_MAX) columns, for a matrix of `bits`-bit
- * values (4 or 2) that is row-reordered when `reordered` != 0 (its stages
- * are larger). Host only; for tuning and reporting. Same argument errors as
- * us_spmm; US_ERR_ARG if no configuration fits.
+ * visible), given a workspace: the paper's split-K (Section VI-C, the
+ * "UnionSparse Kernel" algorithm's split-K batches) as K slices per
+ * workgroup (one wavefront each) and, in k_blocks (may be NULL), K blocks
+ * across workgroups; LTs per chunk or single-pass slice; and payload staging
+ * (1 whole chunk, 2 ring, 3 single pass) of the first slab of
+ * min(N, US_N_MAX) columns, for a matrix of `bits`-bit values (4 or 2) that
+ * is row-reordered when `reordered` != 0 (its stages are larger). The
+ * paper claims a shape-aware kernel selection (Section I, contributions)
+ * without describing it; this is ours. Host only; for tuning and reporting.
+ * Same argument errors as us_spmm; US_ERR_ARG if no configuration fits.
  */
 us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t bits, int32_t reordered, const us_spmm_opts *opts,
-                       int32_t *split_k, int32_t *chunk_lts, int32_t *staging);
+                       int32_t *split_k, int32_t *chunk_lts, int32_t *staging, int32_t *k_blocks);
 
 /*
  * us_spmm_workspace_size - device workspace bytes us_spmm needs for this
- * shape and options (0 today: the split-K sums are combined on chip).
+ * shape and options: the reduction workspace of the paper's split-K
+ * (Section VI-C, "UnionSparse Kernel" algorithm: StoreTile into the
+ * ReductionWorkspace, then Reduction), used when a row block's K range is
+ * split across workgroups (k_blocks > 1): 4 M min(N, 16) bytes of int32
+ * accumulators, then 4 M / 16 bytes of tickets. 0 when no such split is
+ * requested. The workspace must be zero-filled before its first use; every
+ * call leaves it zero-filled again. Calls that may overlap (other streams,
+ * other threads) need workspaces of their own.
  */
 us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, const us_spmm_opts *opts,
                                  size_t *bytes);
@@ -256,7 +294,9 @@ us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, const us_spmm_
  *            fl32(fl32(Y[m][n]) * scale[m]) is written too (the dequant
  *            epilogue is not part of the paper)
  *   y_f32  : device float32, N x M row-major; NULL exactly when scale is NULL
- *   ws     : device workspace of ws_bytes (may be NULL when the size is 0)
+ *   ws     : device workspace of ws_bytes, 4-byte aligned (may be NULL when
+ *            us_spmm_workspace_size reports 0); see us_spmm_workspace_size
+ *            for its contents between calls
  *   opts   : NULL for automatic choices
  *   stream : hipStream_t
  * Argument errors return before launch; a launch error returns US_ERR_DEVICE.

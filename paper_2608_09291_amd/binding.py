@@ -75,7 +75,13 @@ class IEBMEDev(ctypes.Structure):
 
 
 class SpmmOpts(ctypes.Structure):
-    _fields_ = [("split_k", ctypes.c_int32), ("variant", ctypes.c_int32), ("chunk_lts", ctypes.c_int32)]
+    _fields_ = [("split_k", ctypes.c_int32), ("variant", ctypes.c_int32), ("chunk_lts", ctypes.c_int32),
+                ("k_blocks", ctypes.c_int32)]
+
+
+#: us_spmm_opts.variant values
+VARIANT_AUTO, VARIANT_WHOLE, VARIANT_RING, VARIANT_BURST = 0, 1, 2, 3
+K_BLOCKS_MAX = 64   # US_K_BLOCKS_MAX
 
 
 _lib = None
@@ -99,7 +105,7 @@ def lib():
         L.us_spmm_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(SpmmOpts),
                                              ctypes.POINTER(sz)]
         pi32 = ctypes.POINTER(i32)
-        L.us_spmm_plan.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(SpmmOpts), pi32, pi32, pi32]
+        L.us_spmm_plan.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(SpmmOpts), pi32, pi32, pi32, pi32]
         L.us_spmm.argtypes = [ctypes.POINTER(IEBMEDev), vp, i32, vp, vp, vp, vp, sz,
                               ctypes.POINTER(SpmmOpts), vp]
         L.us_gemm_i8.argtypes = [vp, vp, i32, i32, i32, vp, vp]
@@ -263,29 +269,33 @@ def pack_int4(Xt: np.ndarray) -> np.ndarray:
     return np.ascontiguousarray(u[:, 0::2] | (u[:, 1::2] << 4))
 
 
-def workspace_size(M: int, K: int, N: int, split_k: int = 0) -> int:
+def workspace_size(M: int, K: int, N: int, split_k: int = 0, variant: int = 0, chunk_lts: int = 0,
+                   k_blocks: int = 0) -> int:
+    """us_spmm_workspace_size: device bytes us_spmm needs for these options."""
     n = ctypes.c_size_t(0)
-    opts = SpmmOpts(split_k, 0)
+    opts = SpmmOpts(split_k, variant, chunk_lts, k_blocks)
     _check("us_spmm_workspace_size",
            lib().us_spmm_workspace_size(M, K, N, ctypes.byref(opts), ctypes.byref(n)))
     return n.value
 
 
 def spmm_plan(M: int, K: int, N: int, split_k: int = 0, variant: int = 0, reordered: bool = False,
-              bits: int = 4, chunk_lts: int = 0):
-    """us_spmm_plan: (K slices per row block, LTs per chunk, staging 1 whole / 2 ring)."""
-    opts = SpmmOpts(split_k, variant, chunk_lts)
-    a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+              bits: int = 4, chunk_lts: int = 0, k_blocks: int = 0, full: bool = False):
+    """us_spmm_plan: (K slices per workgroup, LTs per chunk or slice, staging 1 whole / 2 ring /
+    3 single pass), and with full=True also the K blocks across workgroups."""
+    opts = SpmmOpts(split_k, variant, chunk_lts, k_blocks)
+    a, b, c, d = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     _check("us_spmm_plan", lib().us_spmm_plan(M, K, N, bits, int(bool(reordered)), ctypes.byref(opts),
-                                              ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
-    return a.value, b.value, c.value
+                                              ctypes.byref(a), ctypes.byref(b), ctypes.byref(c), ctypes.byref(d)))
+    return (a.value, b.value, c.value, d.value) if full else (a.value, b.value, c.value)
 
 
 def spmm(w: DeviceEncoded, x_packed, N: int, y, scale=None, y_f32=None, split_k: int = 0,
-         ws=None, stream=None, wstruct: IEBMEDev = None, variant: int = 0, chunk_lts: int = 0) -> None:
+         ws=None, stream=None, wstruct: IEBMEDev = None, variant: int = 0, chunk_lts: int = 0,
+         k_blocks: int = 0) -> None:
     """us_spmm: y[n, m] = sum_k W[m, k] X[k, n] (+ optional dequant into y_f32)."""
     s = wstruct if wstruct is not None else w.struct()
-    opts = SpmmOpts(split_k, variant, chunk_lts)
+    opts = SpmmOpts(split_k, variant, chunk_lts, k_blocks)
     _check("us_spmm", lib().us_spmm(
         ctypes.byref(s), x_packed.data_ptr(), N, y.data_ptr(),
         None if scale is None else scale.data_ptr(),

@@ -1,6 +1,7 @@
 // Host side of the IE-BME SpMM (Section VI, "UnionSparse Kernel"
-// algorithm): argument checks, the choice of split and chunk configuration,
-// and the launch. The kernel is in us_spmm_kernel.h.
+// algorithm): argument checks, the choice of kernel family, split and chunk
+// configuration, and the launch. The kernels are in us_spmm_kernel.h
+// (chunked) and us_spmm_burst.h (single pass).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -8,6 +9,7 @@
 #include <atomic>
 
 #include "us.h"
+#include "us_spmm_burst.h"
 #include "us_spmm_kernel.h"
 
 namespace {
@@ -17,6 +19,57 @@ using namespace us_spmm_detail;
 bool aligned(const void *ptr, uintptr_t n) { return ((uintptr_t)ptr % n) == 0; }
 
 bool chunk_option_ok(int ch) { return ch == 0 || ch == 4 || ch == 8 || ch == 11 || ch == 16; }
+
+bool burst_ch_ok(int ch) {
+    for (int c : kBurstChs)
+        if (c == ch) return true;
+    return false;
+}
+
+// Staging variants of us_spmm_opts.variant.
+constexpr int kVariantWhole = 1, kVariantRing = 2, kVariantBurst = 3;
+
+// A single-pass (burst) launch: wavefronts per workgroup, LTs per slice
+// (instantiation), K blocks across workgroups.
+struct BurstPlan {
+    int wpg = 0, ch = 0, kblocks = 1;
+};
+
+// Whether a burst plan can run this shape: every wavefront gets 1..ch LTs,
+// at most 16 activation columns, and the stage fits the LDS.
+bool burst_fits(const BurstPlan &b, int nkb, int N, bool perm, int bits) {
+    if (b.wpg < 1 || b.kblocks < 1 || N > 16 || !burst_ch_ok(b.ch)) return false;
+    const int rmin = nkb / b.kblocks, rmax = (nkb + b.kblocks - 1) / b.kblocks;
+    if (rmin < b.wpg) return false;
+    if ((rmax + b.wpg - 1) / b.wpg > b.ch) return false;
+    return burst_lds_bytes(b.ch, N, b.wpg, perm, bits) <= kMaxLds;
+}
+
+// Workspace bytes of a plan with `kblocks` K blocks for M rows and up to
+// `ncols` columns per pass: int32 accumulators, then one ticket per 16-row
+// block (zero between calls).
+size_t burst_ws_bytes(int kblocks, int M, int ncols) {
+    if (kblocks <= 1) return 0;
+    return (size_t)4 * (size_t)M * (size_t)ncols + (size_t)4 * (size_t)(M / 16);
+}
+
+// Burst plan from explicit options (variant 3): split_k wavefronts per
+// workgroup (required), chunk_lts LTs per slice (0: the shortest that fits),
+// k_blocks K blocks (0 or 1: none).
+bool burst_from_opts(const us_spmm_opts &o, int nkb, int N, bool perm, int bits, BurstPlan &b) {
+    b.wpg = o.split_k;
+    b.kblocks = o.k_blocks > 0 ? o.k_blocks : 1;
+    if (b.wpg != 1 && b.wpg != 2 && b.wpg != 4 && b.wpg != 8 && b.wpg != 16) return false;
+    if (o.chunk_lts > 0) {
+        b.ch = o.chunk_lts;
+        return burst_fits(b, nkb, N, perm, bits);
+    }
+    for (int c : kBurstChs) {
+        b.ch = c;
+        if (burst_fits(b, nkb, N, perm, bits)) return true;
+    }
+    return false;
+}
 
 // Wavefronts per workgroup (= K slices per row block) and chunk
 // configuration, by a cost model of the kernel's time per CU, summed over
@@ -97,93 +150,136 @@ int device_cus() {
     return n;
 }
 
+// The launch of one slab of up to US_N_MAX columns: a chunked configuration
+// (us_spmm_kernel.h) or a single-pass one (us_spmm_burst.h).
+struct Plan {
+    bool burst = false;
+    int wpg = 0, cfg = -1;     // chunked: wavefronts per workgroup, kCfgs index
+    BurstPlan b;               // burst
+};
+
+// Options checked once for every entry point.
+us_status check_opts(const us_spmm_opts *o) {
+    if (!o) return US_OK;
+    if (o->variant < 0 || o->variant > kVariantBurst) return US_ERR_ARG;
+    if (o->split_k != 0 && o->split_k != 1 && o->split_k != 2 && o->split_k != 4 && o->split_k != 8 &&
+        o->split_k != 16)
+        return US_ERR_ARG;
+    if (o->k_blocks < 0 || o->k_blocks > US_K_BLOCKS_MAX) return US_ERR_ARG;
+    if (o->variant == kVariantBurst) {
+        if (o->split_k == 0 || (o->chunk_lts != 0 && !burst_ch_ok(o->chunk_lts))) return US_ERR_ARG;
+    } else {
+        if (!chunk_option_ok(o->chunk_lts) || o->k_blocks > 1) return US_ERR_ARG;
+    }
+    return US_OK;
+}
+
+// Plan for one slab of N <= US_N_MAX columns. ws_ok: a workspace was given
+// (a split across workgroups is possible; its size is checked by the caller).
+us_status make_plan(int M, int K, int N, bool perm, int bits, const us_spmm_opts *opts, int n_cu, bool ws_ok,
+                    Plan &pl) {
+    const int nkb = K / US_LT_W;
+    pl = Plan();
+    if (opts && opts->variant == kVariantBurst) {
+        if (!burst_from_opts(*opts, nkb, N, perm, bits, pl.b)) return US_ERR_ARG;
+        if (pl.b.kblocks > 1 && !ws_ok) return US_ERR_ARG;
+        pl.burst = true;
+        return US_OK;
+    }
+    int wpg_only = 0, staging = 0, ch_only = 0;
+    if (opts) {
+        staging = opts->variant;
+        ch_only = opts->chunk_lts;
+        if (opts->split_k != 0) {
+            wpg_only = opts->split_k;
+            while (wpg_only > nkb) wpg_only /= 2;          // at least one LT per slice
+        }
+    }
+    choose_config(M, K, N, perm, bits, n_cu, wpg_only, staging, ch_only, pl.wpg, pl.cfg);
+    return pl.cfg < 0 ? US_ERR_ARG : US_OK;               // no configuration fits LDS
+}
+
+us_status check_shape(int32_t M, int32_t K, int32_t N) {
+    if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
+    if ((uint64_t)M * (uint64_t)K >= (1ull << 32)) return US_ERR_SHAPE;
+    if (N < 1 || N > US_N_LIMIT) return US_ERR_SHAPE;
+    return US_OK;
+}
+
 }  // namespace
 
 extern "C" us_status us_spmm_plan(int32_t M, int32_t K, int32_t N, int32_t bits, int32_t reordered,
-                                  const us_spmm_opts *opts, int32_t *split_k, int32_t *chunk_lts, int32_t *staging) {
+                                  const us_spmm_opts *opts, int32_t *split_k, int32_t *chunk_lts, int32_t *staging,
+                                  int32_t *k_blocks) {
     if (!split_k || !chunk_lts || !staging) return US_ERR_ARG;
     if (bits != 4 && bits != 2) return US_ERR_ARG;
     if (bits == 2 && reordered) return US_ERR_ARG;
-    if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
-    if (N < 1 || N > US_N_LIMIT) return US_ERR_SHAPE;
-    int wpg_only = 0, stg = 0, ch_only = 0;
-    if (opts) {
-        if (opts->variant < 0 || opts->variant > 2) return US_ERR_ARG;
-        if (!chunk_option_ok(opts->chunk_lts)) return US_ERR_ARG;
-        stg = opts->variant;
-        ch_only = opts->chunk_lts;
-        const int s = opts->split_k;
-        if (s != 0) {
-            if (s != 1 && s != 2 && s != 4 && s != 8 && s != 16) return US_ERR_ARG;
-            wpg_only = s;
-            while (wpg_only > K / US_LT_W) wpg_only /= 2;
-        }
+    us_status st = check_shape(M, K, N);
+    if (st != US_OK) return st;
+    if ((st = check_opts(opts)) != US_OK) return st;
+    Plan pl;
+    st = make_plan(M, K, std::min(N, US_N_MAX), reordered != 0, bits, opts, device_cus(), true, pl);
+    if (st != US_OK) return st;
+    if (pl.burst) {
+        *split_k = pl.b.wpg;
+        *chunk_lts = pl.b.ch;
+        *staging = kVariantBurst;
+    } else {
+        *split_k = pl.wpg;
+        *chunk_lts = kCfgs[pl.cfg].ch;
+        *staging = kCfgs[pl.cfg].ring ? kVariantRing : kVariantWhole;
     }
-    int wpg = 0, cfg = -1;
-    choose_config(M, K, std::min(N, US_N_MAX), reordered != 0, bits, device_cus(), wpg_only, stg, ch_only, wpg, cfg);
-    if (cfg < 0) return US_ERR_ARG;
-    *split_k = wpg;
-    *chunk_lts = kCfgs[cfg].ch;
-    *staging = kCfgs[cfg].ring ? 2 : 1;
+    if (k_blocks) *k_blocks = pl.burst ? pl.b.kblocks : 1;
     return US_OK;
 }
 
 extern "C" us_status us_spmm_workspace_size(int32_t M, int32_t K, int32_t N, const us_spmm_opts *opts,
                                             size_t *bytes) {
     if (!bytes) return US_ERR_ARG;
-    if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
-    if (N < 1 || N > US_N_LIMIT) return US_ERR_SHAPE;
-    if (opts && (opts->variant < 0 || opts->variant > 2 || opts->split_k < 0 || !chunk_option_ok(opts->chunk_lts)))
-        return US_ERR_ARG;
-    *bytes = 0;
+    us_status st = check_shape(M, K, N);
+    if (st != US_OK) return st;
+    if ((st = check_opts(opts)) != US_OK) return st;
+    const int kb = (opts && opts->variant == kVariantBurst) ? std::max(1, (int)opts->k_blocks) : 1;
+    *bytes = burst_ws_bytes(kb, M, std::min(N, 16));
     return US_OK;
 }
 
 extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N, int32_t *y,
                              const float *scale, float *y_f32, void *ws, size_t ws_bytes,
                              const us_spmm_opts *opts, void *stream) {
-    (void)ws;
-    (void)ws_bytes;
     if (!w || !x || !y || !w->bitmaps || !w->offsets) return US_ERR_ARG;
     if ((scale == nullptr) != (y_f32 == nullptr)) return US_ERR_ARG;
     const int32_t M = w->M, K = w->K;
-    if (M <= 0 || K <= 0 || M % US_LT_H || K % US_LT_W || K > US_K_MAX) return US_ERR_SHAPE;
-    if ((uint64_t)M * (uint64_t)K >= (1ull << 32)) return US_ERR_SHAPE;
-    if (N < 1 || N > US_N_LIMIT) return US_ERR_SHAPE;
+    us_status st = check_shape(M, K, N);
+    if (st != US_OK) return st;
     const int64_t nkb = K / US_LT_W;
     if (w->n_lt != (int64_t)(M / US_LT_H) * nkb) return US_ERR_FORMAT;
     if (w->n_payload < 0 || w->n_payload > (int64_t)M * K || w->n_payload % 4) return US_ERR_FORMAT;
     if (w->n_payload > 0 && !w->payload) return US_ERR_ARG;
     if (!aligned(w->bitmaps, 8) || !aligned(w->offsets, 4) || !aligned(x, 16) || !aligned(y, 4) ||
-        (scale && (!aligned(scale, 4) || !aligned(y_f32, 4))) || (w->perm && !aligned(w->perm, 8)))
+        (scale && (!aligned(scale, 4) || !aligned(y_f32, 4))) || (w->perm && !aligned(w->perm, 8)) ||
+        !aligned(ws, 4))
         return US_ERR_ARG;
     const bool perm = w->perm != nullptr;
     const int bits = w->bits == 0 ? 4 : w->bits;
     if (bits != 4 && bits != 2) return US_ERR_FORMAT;
     if (bits == 2 && perm) return US_ERR_ARG;              // no reordered 2-bit kernels
+    if ((st = check_opts(opts)) != US_OK) return st;
 
-    int wpg_only = 0, staging = 0, ch_only = 0;
-    if (opts) {
-        if (opts->variant < 0 || opts->variant > 2) return US_ERR_ARG;
-        if (!chunk_option_ok(opts->chunk_lts)) return US_ERR_ARG;
-        staging = opts->variant;
-        ch_only = opts->chunk_lts;
-        const int s = opts->split_k;
-        if (s != 0) {
-            if (s != 1 && s != 2 && s != 4 && s != 8 && s != 16) return US_ERR_ARG;
-            wpg_only = s;
-            while (wpg_only > nkb) wpg_only /= 2;          // at least one LT per slice
-        }
-    }
-    // Slabs of up to US_N_MAX columns: every full slab shares one
-    // configuration, a narrower last slab gets its own. Both are chosen
-    // before anything is launched.
+    // Slabs of up to US_N_MAX columns: every full slab shares one plan, a
+    // narrower last slab gets its own. Both are made before anything is
+    // launched. A split across workgroups needs the workspace for the
+    // slab's columns.
     const int n_cu = device_cus();
     const int n_full = std::min<int>(N, US_N_MAX), n_last = N % US_N_MAX == 0 ? n_full : N % US_N_MAX;
-    int wpg = 0, cfg = -1, wpg_last = 0, cfg_last = -1;
-    choose_config(M, K, n_full, perm, bits, n_cu, wpg_only, staging, ch_only, wpg, cfg);
-    choose_config(M, K, n_last, perm, bits, n_cu, wpg_only, staging, ch_only, wpg_last, cfg_last);
-    if (cfg < 0 || cfg_last < 0) return US_ERR_ARG;        // no configuration fits LDS
+    Plan p_full, p_last;
+    if ((st = make_plan(M, K, n_full, perm, bits, opts, n_cu, ws != nullptr, p_full)) != US_OK) return st;
+    if ((st = make_plan(M, K, n_last, perm, bits, opts, n_cu, ws != nullptr, p_last)) != US_OK) return st;
+    for (const Plan *pl : {&p_full, &p_last}) {
+        if (pl->burst && pl->b.kblocks > 1 &&
+            (ws == nullptr || ws_bytes < burst_ws_bytes(pl->b.kblocks, M, pl == &p_full ? n_full : n_last)))
+            return US_ERR_ARG;
+    }
 
     SpmmArgs a;
     a.bm32 = (const uint32_t *)w->bitmaps;
@@ -203,15 +299,28 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     hipStream_t s = (hipStream_t)stream;
     for (int n0 = 0; n0 < N; n0 += US_N_MAX) {
         const int ns = std::min(US_N_MAX, N - n0);
-        const int sw = ns == n_full ? wpg : wpg_last, sc = ns == n_full ? cfg : cfg_last;
+        const Plan &pl = ns == n_full ? p_full : p_last;
         a.x = x + (int64_t)n0 * (K / 2);
         a.y = y + (int64_t)n0 * M;
         a.yf = y_f32 ? y_f32 + (int64_t)n0 * M : nullptr;
         a.N = ns;
-        const hipError_t err = bits == 2 ? launch_cfg_w2(sw, sc, a, s)
-                               : perm    ? launch_cfg_perm(sw, sc, a, s)
-                               : ns <= 4 ? launch_cfg_narrow(sw, sc, a, s)
-                                         : launch_cfg<false, 4>(sw, sc, a, s);
+        hipError_t err;
+        if (pl.burst) {
+            BurstArgs b;
+            b.a = a;
+            b.kblocks = pl.b.kblocks;
+            b.ws_acc = (int32_t *)ws;
+            b.ws_tick = ws ? (uint32_t *)((char *)ws + (size_t)4 * M * ns) : nullptr;
+            err = bits == 2 ? launch_burst_w2(pl.b.wpg, pl.b.ch, b, s)
+                  : perm    ? launch_burst_perm(pl.b.wpg, pl.b.ch, b, s)
+                  : ns <= 4 ? launch_burst_narrow(pl.b.wpg, pl.b.ch, b, s)
+                            : launch_burst_plain(pl.b.wpg, pl.b.ch, b, s);
+        } else {
+            err = bits == 2 ? launch_cfg_w2(pl.wpg, pl.cfg, a, s)
+                  : perm    ? launch_cfg_perm(pl.wpg, pl.cfg, a, s)
+                  : ns <= 4 ? launch_cfg_narrow(pl.wpg, pl.cfg, a, s)
+                            : launch_cfg<false, 4>(pl.wpg, pl.cfg, a, s);
+        }
         if (err != hipSuccess) return US_ERR_DEVICE;
     }
     return US_OK;

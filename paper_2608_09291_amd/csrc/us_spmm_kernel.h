@@ -71,6 +71,7 @@
 #include <type_traits>
 
 #include "us.h"
+#include "us_range.h"
 
 #ifndef US_SPMM_WINDOW
 #define US_SPMM_WINDOW 2
@@ -238,10 +239,14 @@ __device__ __forceinline__ void wait_vm_all() { wait_vm<0>(); }
 // this one), so nothing of its own lives across the statement.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
+// The LDS base and the scalar offset must be wave-uniform; they are passed
+// through readfirstlane so that they always reach the instruction in scalar
+// registers (a no-op for values the compiler already keeps there).
 __device__ __forceinline__ void dma16(u32x4 desc, uint32_t lds, uint32_t voff, uint32_t soff) {
     __asm__ volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen nt lds"
                      :
-                     : "s"(lds), "v"(voff), "s"(desc), "s"(soff)
+                     : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(desc),
+                       "s"(__builtin_amdgcn_readfirstlane(soff))
                      : "memory", "m0");
 }
 #pragma clang diagnostic pop
@@ -455,17 +460,17 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
         wait_vm_all();                                     // offsets, bitmaps, activations
 
         const uint32_t ob = lane_value(offv, 0), oe = lane_value(offv, cnt);
-        A0 = (ob >> kValShift) & ~15u;                     // first staged payload byte
-        const uint32_t span = ((((oe - (A0 << kValShift)) * (uint32_t)BITS) >> 5) << 2) + 8u;
-        const uint32_t nq = min((span + 15u) >> 4, (uint32_t)C::kPayPieces);
-        // Payload: 16-byte pieces from A0; load u brings stage bytes
-        // [1024 u, 1024 u + 1024). Pieces past the chunk read zero (range
-        // check) and cost no memory traffic. kWindow loads are in flight per
+        // Payload: 16-byte pieces from A0, the first staged byte; load u
+        // brings stage bytes [1024 u, 1024 u + 1024). Pieces past the chunk
+        // read zero (range check) and cost no memory traffic. The range
+        // saturates, so offsets that are not a valid encoding never move the
+        // descriptor outside the payload. kWindow loads are in flight per
         // wavefront, so early pieces are not queued behind the whole
         // machine's requests and decoding starts while the rest streams.
         // Non-temporal: the stream does not displace the activations, which
         // every workgroup re-reads, from L2.
-        const uint32_t prange = min(16u * nq, (uint32_t)p.pay_bytes - A0);
+        A0 = us_range::first_byte<BITS>(ob, (uint32_t)p.pay_bytes);
+        const uint32_t prange = us_range::range_bytes<BITS>(oe, A0, (uint32_t)p.pay_bytes, (uint32_t)C::kPayPieces);
         if constexpr (!kDirect) {
             psrc = __builtin_amdgcn_make_buffer_rsrc((void *)(p.pay + A0), (short)0, (int)prange, kBufferDword3);
         } else {

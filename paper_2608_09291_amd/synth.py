@@ -72,6 +72,10 @@ WORKLOADS = {
             note="the paper's first profiling shape (m=28672, k=7168, batch 8)"),
         _wl("prof_12288x49152_s50", 5, 1, 12288, 49152, 0.5, (4,),
             note="the paper's second profiling shape (m=12288, k=49152, batch 4)"),
+        _wl("kv_1024x4096_s50", 6, 0, 1024, 4096, 0.5, (8,),
+            note="grouped-query key/value projection of an 8B model (8 KV heads of 128)"),
+        _wl("kv_512x3584_s50", 6, 1, 512, 3584, 0.5, (8,),
+            note="grouped-query key/value projection of a 7B model (4 KV heads of 128)"),
     ]
 }
 

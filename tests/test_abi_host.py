@@ -164,7 +164,9 @@ def _dev_struct(M=32, K=128, n_lt=None, n_payload=0, ptr=0x1000):
     ("m_not_16", -2), ("k_not_64", -2), ("k_too_big", -2), ("n_zero", -2), ("n_1025", -2),
     ("n_lt_wrong", -6), ("payload_odd", -6), ("payload_too_big", -6),
     ("split_3", -1), ("variant", -1), ("misaligned_x", -1), ("misaligned_perm", -1),
-    ("bits_3", -6), ("bits_2_reordered", -1)])
+    ("bits_3", -6), ("bits_2_reordered", -1), ("single_pass_no_split", -1), ("k_blocks_chunked", -1),
+    ("k_blocks_no_ws", -1), ("k_blocks_small_ws", -1), ("k_blocks_65", -1), ("single_pass_n17", -1),
+    ("single_pass_ch_5", -1), ("misaligned_ws", -1)])
 def test_spmm_argument_errors_before_launch(case, status):
     """Every argument error returns before touching the GPU (pointers are fake)."""
     L = binding.lib()
@@ -173,6 +175,7 @@ def test_spmm_argument_errors_before_launch(case, status):
     N = 8
     opts = binding.SpmmOpts(0, 0)
     wp = ctypes.byref(w)
+    ws, ws_bytes = None, 0
     if case == "null_w":
         wp = None
     elif case == "null_x":
@@ -201,7 +204,26 @@ def test_spmm_argument_errors_before_launch(case, status):
     elif case == "split_3":
         opts.split_k = 3
     elif case == "variant":
+        opts.variant = 4
+    elif case == "single_pass_no_split":           # the single pass needs an explicit split
         opts.variant = 3
+    elif case == "k_blocks_chunked":               # K blocks across workgroups: single pass only
+        opts.k_blocks = 2
+    elif case == "k_blocks_no_ws":
+        opts.split_k, opts.variant, opts.k_blocks = 1, 3, 2
+    elif case == "k_blocks_small_ws":
+        opts.split_k, opts.variant, opts.k_blocks = 1, 3, 2
+        ws, ws_bytes = 0x6000, 4 * 32 * 8
+    elif case == "k_blocks_65":
+        opts.split_k, opts.variant, opts.k_blocks = 1, 3, 65
+        ws, ws_bytes = 0x6000, 1 << 20
+    elif case == "single_pass_n17":
+        opts.split_k, opts.variant = 1, 3
+        N = 17
+    elif case == "single_pass_ch_5":
+        opts.split_k, opts.variant, opts.chunk_lts = 1, 3, 5
+    elif case == "misaligned_ws":
+        ws, ws_bytes = 0x6002, 1 << 20
     elif case == "misaligned_x":
         x = 0x2002
     elif case == "misaligned_perm":
@@ -210,7 +232,7 @@ def test_spmm_argument_errors_before_launch(case, status):
         w.bits = 3
     elif case == "bits_2_reordered":
         w.bits, w.perm = 2, 0x5000
-    got = L.us_spmm(wp, x, N, y, sc, yf, None, 0, ctypes.byref(opts), None)
+    got = L.us_spmm(wp, x, N, y, sc, yf, ws, ws_bytes, ctypes.byref(opts), None)
     assert got == status
 
 
@@ -222,10 +244,18 @@ def test_gemm_argument_errors():
     assert L.us_gemm_i8(0x18, 0x10, 16, 64, 1, 0x20, None) == -1
 
 
-def test_workspace_size_is_zero():
+def test_workspace_size():
+    # No workspace unless the K range is split across workgroups; then int32
+    # accumulators for min(N, 16) columns and one ticket per 16-row block.
     assert binding.workspace_size(4096, 11008, 8) == 0
+    assert binding.workspace_size(4096, 11008, 8, split_k=4, variant=3) == 0
+    for N in (1, 8, 16, 32):
+        assert binding.workspace_size(4096, 11008, N, split_k=4, variant=3, k_blocks=4) == \
+            4 * 4096 * min(N, 16) + 4 * 256
     with pytest.raises(binding.UsError):
         binding.workspace_size(4096, 11008, 0)
+    with pytest.raises(binding.UsError):
+        binding.workspace_size(4096, 11008, 8, k_blocks=2)          # needs the single pass
 
 
 def test_probe_argument_errors():
@@ -286,14 +316,44 @@ def test_plan_invariants(M, K, N, reordered):
 
 def test_plan_argument_errors():
     L = binding.lib()
-    a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    a, b, c, d = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     ok = ctypes.byref(binding.SpmmOpts(0, 0))
-    assert L.us_spmm_plan(32, 128, 8, 4, 0, ok, None, ctypes.byref(b), ctypes.byref(c)) == -1
-    assert L.us_spmm_plan(40, 128, 8, 4, 0, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
-    assert L.us_spmm_plan(32, 128, 1025, 4, 1, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -2
+    ra, rb, rc, rd = ctypes.byref(a), ctypes.byref(b), ctypes.byref(c), ctypes.byref(d)
+    assert L.us_spmm_plan(32, 128, 8, 4, 0, ok, None, rb, rc, rd) == -1
+    assert L.us_spmm_plan(40, 128, 8, 4, 0, ok, ra, rb, rc, rd) == -2
+    assert L.us_spmm_plan(32, 128, 1025, 4, 1, ok, ra, rb, rc, rd) == -2
     bad = ctypes.byref(binding.SpmmOpts(3, 0))
-    assert L.us_spmm_plan(32, 128, 8, 4, 0, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(32, 128, 8, 4, 0, bad, ra, rb, rc, rd) == -1
     bad = ctypes.byref(binding.SpmmOpts(0, 5))
-    assert L.us_spmm_plan(32, 128, 8, 4, 1, bad, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
-    assert L.us_spmm_plan(32, 128, 8, 3, 0, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
-    assert L.us_spmm_plan(32, 128, 8, 2, 1, ok, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)) == -1
+    assert L.us_spmm_plan(32, 128, 8, 4, 1, bad, ra, rb, rc, rd) == -1
+    assert L.us_spmm_plan(32, 128, 8, 3, 0, ok, ra, rb, rc, rd) == -1
+    assert L.us_spmm_plan(32, 128, 8, 2, 1, ok, ra, rb, rc, rd) == -1
+    # The K-block output may be omitted.
+    assert L.us_spmm_plan(32, 128, 8, 4, 0, ok, ra, rb, rc, None) == 0
+
+
+@pytest.mark.parametrize("bits,reordered", [(4, False), (4, True), (2, False)])
+@pytest.mark.parametrize("M,K", [(16, 64), (512, 512), (1024, 4096), (4096, 11008)])
+@pytest.mark.parametrize("N", [1, 8, 16])
+def test_single_pass_plans(M, K, N, bits, reordered):
+    """Single-pass plans (variant 3): every wavefront gets 1..ch LTs of its
+    workgroup's K block, the stage fits the LDS, and the plan echoes the
+    forced choices; impossible ones are refused."""
+    nkb = K // 64
+    accepted = 0
+    for split in (1, 2, 4, 8, 16):
+        for kb in (1, 2, 4, 8):
+            for ch in (0, 4, 8, 11, 16, 22, 32):
+                rmin, rmax = nkb // kb, -(-nkb // kb)
+                try:
+                    s, c, stg, k = binding.spmm_plan(M, K, N, split, 3, reordered, bits, ch, kb, full=True)
+                except binding.UsError:
+                    # Refused: no slice length fits, or the stage does not fit the LDS.
+                    continue
+                accepted += 1
+                assert (s, stg, k) == (split, 3, kb)
+                assert c in (4, 8, 11, 16, 22, 32) and (ch == 0 or c == ch)
+                assert rmin >= split and -(-rmax // split) <= c
+                if ch == 0:      # the shortest slice length that holds every wavefront's LTs
+                    assert all(-(-rmax // split) > c2 for c2 in (4, 8, 11, 16, 22, 32) if c2 < c)
+    assert accepted > 0

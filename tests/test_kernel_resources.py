@@ -21,7 +21,8 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2608_09291_amd", "csrc")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-UNITS = ("us_spmm", "us_spmm_narrow", "us_spmm_perm", "us_spmm_w2")
+UNITS = ("us_spmm", "us_spmm_narrow", "us_spmm_perm", "us_spmm_w2", "us_spmm_burst_plain", "us_spmm_burst_narrow",
+         "us_spmm_burst_perm", "us_spmm_burst_w2")
 FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fno-strict-aliasing", "-Xclang", "-target-feature",
          "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"), "-I", CSRC, "--cuda-device-only", "-S"]
 
@@ -63,8 +64,17 @@ def kernels():
             if "m0" in ln and not ln.startswith(";") and not ln.startswith("."):
                 m0_lines.append((ln, lines[i + 1] if i + 1 < len(lines) else "", lines[i + 2] if i + 2 < len(lines) else ""))
     found = []
+    burst = []
     for text in texts:
         for m in re.finditer(r"\.amdhsa_kernel (\S+)(.*?)\.end_amdhsa_kernel", text, re.S):
+            b = re.search(r"us_spmm_burst_kernelILi(\d+)ELi(\d+)ELi(\d+)ELb(\d)ELi(\d)ELi(\d+)E", m.group(1))
+            if b:
+                wpg, nmax, ch, perm, bits, win = (int(v) for v in b.groups())
+                burst.append(dict(wpg=wpg, nmax=nmax, ch=ch, perm=bool(perm), bits=bits, win=win,
+                                  vgpr=int(re.search(r"\.amdhsa_next_free_vgpr (\d+)", m.group(2)).group(1)),
+                                  scratch=int(re.search(r"\.amdhsa_private_segment_fixed_size (\d+)",
+                                                        m.group(2)).group(1))))
+                continue
             g = re.search(r"us_spmm_kernelILi(\d+)ELi(\d+)ELi(\d+)ELb(\d)ELb(\d)ELb(\d)ELi(\d)E", m.group(1))
             if not g:
                 continue
@@ -73,7 +83,7 @@ def kernels():
             scratch = int(re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", m.group(2)).group(1))
             found.append(dict(wpg=wpg, nmax=nmax, ch=ch, multi=bool(multi), ring=bool(ring), perm=bool(perm),
                               bits=bits, vgpr=vgpr, scratch=scratch))
-    return found, m0_lines
+    return found, m0_lines, burst
 
 
 @pytest.fixture(scope="module")
@@ -81,14 +91,30 @@ def kernel_list(kernels):
     return kernels[0]
 
 
+def burst_waves_per_simd(wpg, nmax):
+    return (6 if wpg >= 4 else 5) if nmax > 4 else (7 if wpg >= 4 else 6)
+
+
 def test_m0_is_only_the_direct_payload_loads(kernels):
-    # The direct payload load sets M0 in assembly and lists it as clobbered;
-    # that is only sound while the compiler itself keeps nothing in M0.
+    # The direct-to-LDS loads set M0 in assembly and list it as clobbered;
+    # that is only sound while the compiler itself keeps nothing in M0. The
+    # LDS base must come from a scalar register: a vector register there
+    # (a value the compiler did not prove wave-uniform) would not be a valid
+    # M0 source, so every write is checked to name an SGPR.
     m0 = kernels[1]
     assert m0, "no direct payload loads found"
     for ln, nxt, nxt2 in m0:
-        assert ln.startswith("s_mov_b32 m0,"), ln
-        assert nxt == "s_nop 0" and nxt2.startswith("buffer_load_dwordx4") and nxt2.endswith(" lds"), (ln, nxt, nxt2)
+        assert re.fullmatch(r"s_mov_b32 m0, s\d+", ln), ln
+        assert nxt == "s_nop 0" and re.match(r"buffer_load_dword(x4)? v\d+, s\[\d+:\d+\], (s\d+|0) offen", nxt2) \
+            and nxt2.endswith(" lds"), (ln, nxt, nxt2)
+
+
+def test_single_pass_kernels_fit_their_residency(kernels):
+    burst = kernels[2]
+    assert len(burst) >= 4 * 5 * 6, len(burst)       # 4 families x 5 WPG x 6 slice lengths
+    over = [k for k in burst if k["vgpr"] > (512 // burst_waves_per_simd(k["wpg"], k["nmax"])) // 8 * 8]
+    assert not over, over[:5]
+    assert not [k for k in burst if k["scratch"]]
 
 
 def test_every_configuration_is_built(kernel_list):
