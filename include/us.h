@@ -308,6 +308,27 @@ us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N, int32_t *y
                   const float *scale, float *y_f32, void *ws, size_t ws_bytes,
                   const us_spmm_opts *opts, void *stream);
 
+/* Bytes of the array us_spmm_noalloc uses as its workspace. */
+#define US_NOALLOC_SCRATCH_BYTES (4u << 20)
+
+/*
+ * us_spmm_noalloc - us_spmm for callers that cannot allocate device memory
+ * or pass a workspace: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc. Same arguments, results and errors as
+ * us_spmm, without ws / ws_bytes: the reduction workspace of a K range split
+ * across workgroups (us_spmm_opts.k_blocks > 1) is a fixed array of
+ * US_NOALLOC_SCRATCH_BYTES bytes inside the library, one per GPU, held until
+ * the process ends. A split whose workspace (us_spmm_workspace_size) exceeds
+ * it returns US_ERR_SHAPE before any launch; US_ERR_DEVICE if the array's
+ * address cannot be obtained. The array is zero when the library is loaded
+ * and every call leaves it zero again, so no call clears it. All calls on
+ * one GPU share that GPU's array: calls that may overlap (several streams or
+ * threads) race on it and must not be issued concurrently. The call itself
+ * allocates nothing.
+ */
+us_status us_spmm_noalloc(const us_iebme_dev *w, const uint8_t *x, int32_t N, int32_t *y,
+                          const float *scale, float *y_f32, const us_spmm_opts *opts, void *stream);
+
 /*
  * us_gemm_i8 - dense INT8 GEMM, Y = W X with INT32 accumulation, on the int8
  * matrix cores: the in-library dense comparison point (the paper compares

@@ -25,7 +25,7 @@ N_LIMIT = 1024      # widest activation matrix (slabs of N_MAX beyond N_MAX)
 K_MAX = 130048
 
 #: Every symbol the two public headers declare.
-EXPORTS = ("us_encode", "us_encode_w2", "us_encode_reordered", "us_iebme_free", "us_pmr", "us_pmr_formats", "us_spmm_plan", "us_spmm_workspace_size", "us_spmm",
+EXPORTS = ("us_encode", "us_encode_w2", "us_encode_reordered", "us_iebme_free", "us_pmr", "us_pmr_formats", "us_spmm_plan", "us_spmm_workspace_size", "us_spmm", "us_spmm_noalloc",
            "us_gemm_i8", "us_status_string", "us_probe_read", "us_probe_read_sink_words",
            "us_probe_copy", "us_probe_spin")
 
@@ -108,6 +108,7 @@ def lib():
         L.us_spmm_plan.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(SpmmOpts), pi32, pi32, pi32, pi32]
         L.us_spmm.argtypes = [ctypes.POINTER(IEBMEDev), vp, i32, vp, vp, vp, vp, sz,
                               ctypes.POINTER(SpmmOpts), vp]
+        L.us_spmm_noalloc.argtypes = [ctypes.POINTER(IEBMEDev), vp, i32, vp, vp, vp, ctypes.POINTER(SpmmOpts), vp]
         L.us_gemm_i8.argtypes = [vp, vp, i32, i32, i32, vp, vp]
         L.us_status_string.argtypes = [ctypes.c_int]
         L.us_status_string.restype = ctypes.c_char_p
@@ -116,7 +117,7 @@ def lib():
         L.us_probe_read_sink_words.restype = sz
         L.us_probe_copy.argtypes = [vp, vp, sz, vp]
         L.us_probe_spin.argtypes = [ctypes.c_uint64, vp]
-        for name in ("us_encode", "us_encode_w2", "us_encode_reordered", "us_pmr", "us_pmr_formats", "us_spmm_workspace_size", "us_spmm_plan", "us_spmm", "us_gemm_i8",
+        for name in ("us_encode", "us_encode_w2", "us_encode_reordered", "us_pmr", "us_pmr_formats", "us_spmm_workspace_size", "us_spmm_plan", "us_spmm", "us_spmm_noalloc", "us_gemm_i8",
                      "us_probe_read", "us_probe_copy", "us_probe_spin"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -301,6 +302,22 @@ def spmm(w: DeviceEncoded, x_packed, N: int, y, scale=None, y_f32=None, split_k:
         None if scale is None else scale.data_ptr(),
         None if y_f32 is None else y_f32.data_ptr(),
         None if ws is None else ws.data_ptr(), 0 if ws is None else ws.numel() * ws.element_size(),
+        ctypes.byref(opts), _stream_handle(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 4 << 20   # US_NOALLOC_SCRATCH_BYTES
+
+
+def spmm_noalloc(w: DeviceEncoded, x_packed, N: int, y, scale=None, y_f32=None, split_k: int = 0,
+                 stream=None, wstruct: IEBMEDev = None, variant: int = 0, chunk_lts: int = 0,
+                 k_blocks: int = 0) -> None:
+    """us_spmm_noalloc: us_spmm with the library's own per-device workspace."""
+    s = wstruct if wstruct is not None else w.struct()
+    opts = SpmmOpts(split_k, variant, chunk_lts, k_blocks)
+    _check("us_spmm_noalloc", lib().us_spmm_noalloc(
+        ctypes.byref(s), x_packed.data_ptr(), N, y.data_ptr(),
+        None if scale is None else scale.data_ptr(),
+        None if y_f32 is None else y_f32.data_ptr(),
         ctypes.byref(opts), _stream_handle(stream)))
 
 

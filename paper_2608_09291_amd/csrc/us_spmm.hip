@@ -325,3 +325,46 @@ extern "C" us_status us_spmm(const us_iebme_dev *w, const uint8_t *x, int32_t N,
     }
     return US_OK;
 }
+
+// The reduction workspace of us_spmm_noalloc: one array per device that the
+// library's code object is loaded on, zero when it is loaded. Host code never
+// uses the array's name as an address: the per-device address comes from
+// hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[US_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current); nullptr if the lookup fails.
+void *scratch_address() {
+    static std::atomic<void *> addr[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    void *p = addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        void *q = nullptr;
+        if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess || !q) return nullptr;
+        addr[dev].store(q, std::memory_order_release);
+        p = q;
+    }
+    return p;
+}
+
+}  // namespace
+
+extern "C" us_status us_spmm_noalloc(const us_iebme_dev *w, const uint8_t *x, int32_t N, int32_t *y,
+                                     const float *scale, float *y_f32, const us_spmm_opts *opts, void *stream) {
+    // The arguments are checked by us_spmm; only the workspace is ours: it
+    // must fit the array (us_spmm refuses a plan whose workspace exceeds
+    // the bytes it is given, before launching anything).
+    if (!w) return US_ERR_ARG;
+    const us_status st = check_shape(w->M, w->K, N);
+    if (st != US_OK) return st;
+    size_t need = 0;
+    if (check_opts(opts) == US_OK && opts && opts->variant == kVariantBurst && opts->k_blocks > 1 &&
+        (need = burst_ws_bytes(opts->k_blocks, w->M, std::min<int>(N, 16))) > US_NOALLOC_SCRATCH_BYTES)
+        return US_ERR_SHAPE;
+    void *ws = scratch_address();
+    if (!ws) return US_ERR_DEVICE;
+    return us_spmm(w, x, N, y, scale, y_f32, ws, US_NOALLOC_SCRATCH_BYTES, opts, stream);
+}
