@@ -99,7 +99,7 @@ void choose_config(int M, int K, int N, bool perm, int bits, int n_cu, int wpg_o
     wpg = 0;
     cfg = -1;
     // Activation width the instantiation is built for (us_spmm's dispatch).
-    const int nmax = N > 16 ? 32 : (N <= 4 && bits == 4 && !perm) ? 4 : 16;
+    const int nmax = N > 16 ? 32 : (N <= 4 && bits == 4) ? 4 : 16;
     for (int w = 16; w >= 1; w /= 2) {
         if (w > nkb || (wpg_only > 0 && w != wpg_only)) continue;
         for (int idx = 0; idx < kNumCfgs; ++idx) {

@@ -50,7 +50,12 @@
 //    pi[8 + i]. The MFMA rows keep the original row order (the accumulator
 //    is shared by all LTs of a row block), so PERM kernels route each
 //    reordered row's row base and mask row to the lane row of its original
-//    row while computing the row bases; the decode itself is unchanged.
+//    row while computing the row bases. The routed values overwrite the
+//    LT's own bitmap and row-base areas of the stage (16-bit row bases in
+//    the bitmap area, two LTs to a dword, the routed mask row in the
+//    row-base area, where the permutation word was staged), so a reordered
+//    stage is exactly as large as a plain one and takes the same
+//    configurations.
 //
 //  * INT4 -> INT8. CDNA4 has no INT4 matrix instruction. Weights and
 //    activations are expanded to bytes that hold the value in the high
@@ -136,9 +141,11 @@ __device__ inline u32x2 perm_selectors(uint32_t m) {
 //   sd      : per LT, the number of bits of one area stream,
 //             BITS (o_{t+1} - o_t) / 4;
 //   offsets : o_t of the chunk's LTs and the end offset (CH + 1 dwords);
-//   perm    : (PERM only) the row permutation word of each LT, 8 bytes;
-//   rows    : (PERM only) per LT and lane row, the union-mask row that lane
-//             row decodes (16 dwords per LT);
+//   (PERM: the bases area of LT j first holds its permutation word; after
+//   the row-base step the bitmap area holds per LT pair and lane row the two
+//   16-bit row bases, stage-relative bit addresses divided by 4, LT 2m in
+//   the low and LT 2m + 1 in the high half of the pair's dword, and the
+//   bases area the union-mask row that lane row decodes)
 //   X       : the chunk's activation slice, one row of 32 bytes per LT for
 //             each activation column; rows are 16 bytes longer than the
 //             slice so that the 16 rows read by one instruction fall in
@@ -155,10 +162,9 @@ struct Chunk {
     static constexpr int kBaseOffset = kBmOffset + 32 * kLtPad;
     static constexpr int kSdOffset = kBaseOffset + 64 * kLtPad;
     static constexpr int kOffOffset = kSdOffset + 4 * kLtPad;
-    static constexpr int kPermOffset = (kOffOffset + 4 * (kLtPad + 1) + 7) & ~7;
-    static constexpr int kRowOffset = kPermOffset + (PERM ? 8 * kLtPad : 0);
-    static constexpr int kXOffset = (kRowOffset + (PERM ? 64 * kLtPad : 0) + 15) & ~15;
-    static constexpr int kRowDelta = kRowOffset - kBaseOffset;   // rows entry of a lane row vs its base
+    static constexpr int kXOffset = (kOffOffset + 4 * (kLtPad + 1) + 15) & ~15;
+    static_assert(!PERM || 8 * (RING ? kRing + kGuard : 16 * kPayPieces) <= 4 * 65536,
+                  "16-bit row bases address the payload stage");
     static constexpr int kXRowWords = 8 * CH + 4;
     static constexpr int kXPieces = 2 * CH;                   // 16-byte pieces of one activation row
     static_assert(2 * CH <= 64, "bitmap rows: one 16-byte load per half LT");
@@ -185,14 +191,14 @@ struct SpmmArgs {
 // 64 VGPRs with four or more wavefronts per workgroup, 72 above 16
 // activation columns, 80 with fewer wavefronts);
 // multi-chunk slices also hold the next chunk's inputs, more of them for
-// longer chunks and wider activation tiles, and ring staging, like every
-// kernel above 16 activation columns, holds the payload pieces in flight in
-// registers.
-constexpr int waves_per_simd(int wpg, int nmax, int ch, bool multi, bool ring, [[maybe_unused]] bool perm) {
+// longer chunks and wider activation tiles (and, for reordered LTs, their
+// permutation words), and ring staging, like every kernel above 16
+// activation columns, holds the payload pieces in flight in registers.
+constexpr int waves_per_simd(int wpg, int nmax, int ch, bool multi, bool ring, bool perm) {
     return nmax > 16   ? (multi ? 4 : wpg >= 4 ? 7 : 6)
            : !multi    ? (wpg >= 4 ? 8 : 6)
            : ring      ? (nmax <= 4 ? 5 : 4)
-           : nmax <= 4 ? 7
+           : nmax <= 4 ? (perm && ch > 11 ? 6 : 7)
                        : (ch <= 4 ? 7 : ch <= 11 ? 5 : 4);
 }
 
@@ -208,6 +214,8 @@ __device__ __forceinline__ uint32_t lds_load(uint32_t addr) { return *(const lds
 // Two consecutive dwords at a 4-byte aligned address.
 __device__ __forceinline__ uint2 lds_load2(uint32_t addr) { return make_uint2(lds_load(addr), lds_load(addr + 4)); }
 __device__ __forceinline__ void lds_store(uint32_t addr, uint32_t v) { *(lds_u32 *)(size_t)addr = v; }
+typedef __attribute__((address_space(3))) uint16_t lds_u16;
+__device__ __forceinline__ void lds_store16(uint32_t addr, uint16_t v) { *(lds_u16 *)(size_t)addr = v; }
 __device__ __forceinline__ void lds_store2(uint32_t addr, u32x2 v) { *(lds_u2 *)(size_t)addr = v; }
 __device__ __forceinline__ void lds_store4(uint32_t addr, u32x4 v) { *(lds_u4 *)(size_t)addr = v; }
 
@@ -295,14 +303,13 @@ __device__ __forceinline__ int2 place2(uint32_t w, uint2 sel) {
 
 // Decode one LT into the MFMA A operand of this lane.
 //   mrow : union-mask row i of the LT
-//   base : LDS bit address of row i's first value in area stream 2a
+//   bn0  : LDS bit address of the first value of the lane's segment of row
+//          i in area stream 2a
 //   sd   : bits of one area stream (stream 2a + 1 starts sd bits later)
 //   rot  : (8 g - 3) mod 32, so that rotating mrow right by it puts the
 //          lane's segment at bits 3..10 (the selector table's byte offset)
 template <int BITS>
-__device__ __forceinline__ i32x4 decode_tile(const u32x2 *lut, uint32_t mrow, uint32_t base, uint32_t sd,
-                                             uint32_t lomask, uint32_t rot) {
-    const uint32_t bn0 = base + (uint32_t)BITS * __popc(mrow & lomask);
+__device__ __forceinline__ i32x4 decode_at(const u32x2 *lut, uint32_t mrow, uint32_t bn0, uint32_t sd, uint32_t rot) {
     const uint32_t bn1 = bn0 + sd;
     const u32x2 sv = *(const u32x2 *)((const char *)lut + (__builtin_amdgcn_alignbit(mrow, mrow, rot) & 0x7F8u));
     const uint2 sel = make_uint2(sv.x, sv.y);
@@ -315,6 +322,22 @@ __device__ __forceinline__ i32x4 decode_tile(const u32x2 *lut, uint32_t mrow, ui
         c1 = place2(window(bn1), sel);
     }
     return (i32x4){c0.x, c0.y, c1.x, c1.y};
+}
+
+// The same from the row's base: the segment starts BITS x (active positions
+// of the row before it) bits further on.
+template <int BITS>
+__device__ __forceinline__ i32x4 decode_tile(const u32x2 *lut, uint32_t mrow, uint32_t base, uint32_t sd,
+                                             uint32_t lomask, uint32_t rot) {
+    return decode_at<BITS>(lut, mrow, base + (uint32_t)BITS * __popc(mrow & lomask), sd, rot);
+}
+
+// The same for a 4-bit row base given as a stage-relative bit address / 4
+// (q) and the stage's bit address st8: the segment starts at
+// st8 + 4 (q + active positions before it).
+__device__ __forceinline__ i32x4 decode_tile_q(const u32x2 *lut, uint32_t mrow, uint32_t q, uint32_t st8, uint32_t sd,
+                                               uint32_t lomask, uint32_t rot) {
+    return decode_at<4>(lut, mrow, st8 + ((q + (uint32_t)__popc(mrow & lomask)) << 2), sd, rot);
 }
 
 // Dwords g and g + 4 of an activation row's 8 dwords for one LT.
@@ -342,6 +365,7 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     constexpr int NB = NMAX > 16 ? 2 : 1;                 // MFMA column blocks
     using C = Chunk<CH, RING, PERM, BITS>;
     static_assert(BITS == 4 || BITS == 2, "payload values are 4 or 2 bits");
+    static_assert(!PERM || BITS == 4, "16-bit row bases hold stage bit addresses / 4 (4-bit values)");
     constexpr int kValShift = BITS == 4 ? 1 : 2;          // log2(values per byte)
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
     __shared__ u32x2 lut[256];                               // selector table
@@ -372,7 +396,6 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     const uint32_t st = lds0 + (uint32_t)(wave * stage_bytes);   // stage, LDS bytes
     const uint32_t st_bm = st + C::kBmOffset, st_base = st + C::kBaseOffset;
     const uint32_t st_sd = st + C::kSdOffset, st_off = st + C::kOffOffset;
-    const uint32_t st_pm = st + C::kPermOffset;
     const uint32_t st_x = st + C::kXOffset;
 
     // Activation reads in the decode: lane (column rr, k-group g) reads dwords
@@ -409,7 +432,7 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     // into the matrix.
     uint32_t offv;
     u32x4 pbm;
-    [[maybe_unused]] u32x2 pperm;
+    [[maybe_unused]] u32x2 pperm;                        // (PERM) lane j: word of the chunk's LT j
     i32x4 px[kXLoads];
     auto request = [&](int c0) {
         const int cnt = min(CH, nlt - c0);                 // >= 1
@@ -490,7 +513,11 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
             if (lane < 2 * CH) lds_store4(st_bm + 16 * lane, lane < 2 * cnt ? pbm : (u32x4){0u, 0u, 0u, 0u});
             if (lane <= CH) lds_store(st_off + 4 * lane, offv);
             if constexpr (PERM) {
-                if (lane < CH) lds_store2(st_pm + 8 * lane, pperm);
+                // The lane row of original row r is 2 (r mod 8) + r / 8,
+                // r's 4 bits rotated left by one: done here for every
+                // nibble at once.
+                auto lane_rows = [](uint32_t w) { return ((w << 1) & 0xEEEEEEEEu) | ((w >> 3) & 0x11111111u); };
+                if (lane < CH) lds_store2(st_base + 64 * lane, (u32x2){lane_rows(pperm.x), lane_rows(pperm.y)});
             }
 #pragma unroll
             for (int u = 0; u < kXLoads; ++u)
@@ -516,7 +543,11 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
         // a = 1 at 2 P_t (its streams follow streams 0 and 1) and adds the
         // popcounts of the rows before i. With PERM the row base and the
         // mask row of (i, a), i.e. of reordered row 8a + i, go to the lane
-        // row of original row r = pi[8a + i]: 2 (r mod 8) + r / 8.
+        // row of original row r = pi[8a + i]: 2 (r mod 8) + r / 8; the row
+        // base (as a 16-bit stage bit address / 4) into the LT pair's bitmap
+        // area, the mask row into the LT's bases area. Every bitmap and
+        // permutation word of the chunk is read before the first of them is
+        // overwritten.
         // Payload value v of the matrix is stream bit BITS v - 8 A0, at LDS
         // bit address 8 st + (BITS v - 8 A0), taken mod 32768 with the ring.
         const uint32_t rmask = RING ? 0x7FFFu : ~0u;
@@ -524,7 +555,8 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
             const uint32_t jj = (uint32_t)lane >> 4;
             const uint32_t p_bm = st_bm + 32 * jj + 4 * i, p_off = st_off + 4 * jj;
             const uint32_t q_base = st_base + 64 * jj, p_base = q_base + 4 * rr, p_sd = st_sd + 4 * jj;
-            const uint32_t p_pm = st_pm + 8 * jj + 4 * (rr & 1);
+            const uint32_t q_b16 = st_bm + 64 * (jj >> 1) + 2 * (jj & 1), p_b16 = q_b16 + 4 * rr;
+            const uint32_t p_pm = q_base + 4 * (rr & 1);
             uint32_t mrow[C::kPasses];
             uint2 o[C::kPasses];
             [[maybe_unused]] uint32_t pm[C::kPasses];
@@ -532,7 +564,7 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
             for (int ps = 0; ps < C::kPasses; ++ps) {
                 mrow[ps] = lds_load(p_bm + 128 * ps);
                 o[ps] = lds_load2(p_off + 16 * ps);
-                if constexpr (PERM) pm[ps] = lds_load(p_pm + 32 * ps);   // pi[8a .. 8a + 7]
+                if constexpr (PERM) pm[ps] = lds_load(p_pm + 256 * ps);   // lane rows of pi[8a .. 8a + 7], LT 4 ps + jj
             }
 #pragma unroll
             for (int ps = 0; ps < C::kPasses; ++ps) {
@@ -542,17 +574,20 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
                 ex += dpp_row<0x112>(ex);
                 ex += dpp_row<0x114>(ex);
                 ex += dpp_row<0x118>(ex);
-                const uint32_t bval = 8u * st + (((uint32_t)BITS * (o[ps].x + ex) - 8u * A0) & rmask);
-                lds_store(p_base + 256 * ps, bval);
                 if constexpr (PERM) {
-                    // This lane's own lane row is written first, so that a
-                    // word that is not a permutation still leaves every lane
-                    // row with an address inside the stage.
-                    const uint32_t r = (pm[ps] >> (4 * i)) & 15u;
-                    const uint32_t slot = 4u * (((r & 7u) << 1) | (r >> 3));
-                    lds_store(p_base + 256 * ps + C::kRowDelta, mrow[ps]);
-                    lds_store(q_base + 256 * ps + slot, bval);
-                    lds_store(q_base + 256 * ps + slot + C::kRowDelta, mrow[ps]);
+                    // The base is first written under this lane's own lane
+                    // row, so that a word that is not a permutation still
+                    // leaves every lane row with a base inside the stage.
+                    // (16 bits hold rel / 4: rel is a multiple of 4 below 8
+                    // x the payload area.)
+                    const uint32_t lr = (pm[ps] >> (4 * i)) & 15u;
+                    const uint16_t b16 = (uint16_t)((o[ps].x + ex - 2u * A0) & (rmask >> 2));   // rel / 4
+                    lds_store16(p_b16 + 128 * ps, b16);
+                    lds_store(q_base + 4 * lr + 256 * ps, mrow[ps]);
+                    lds_store16(q_b16 + 4 * lr + 128 * ps, b16);
+                } else {
+                    const uint32_t rel = ((uint32_t)BITS * (o[ps].x + ex) - 8u * A0) & rmask;
+                    lds_store(p_base + 256 * ps, 8u * st + rel);
                 }
                 if (rr == 0) lds_store(p_sd + 16 * ps, ((o[ps].y - o[ps].x) * (uint32_t)BITS) >> 2);
             }
@@ -566,41 +601,51 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
         // activations for this lane; they advance as LTs are decoded. The
         // stream-length address is the same on every lane; it is kept in a
         // vector register so that the loop needs no scalar-to-vector moves.
-        // PERM reads the mask row routed to this lane row, which sits at a
-        // fixed distance from the row base (no pointer of its own).
-        uint32_t a_bm = st_bm + 4 * i, a_base = st_base + 4 * rr, a_sd;
-        auto row_at = [&](int k) { return PERM ? a_base + 64 * k + C::kRowDelta : a_bm + 32 * k; };
+        // PERM reads the mask row routed to this lane row from the bases
+        // area and the 16-bit row bases of an LT pair from one dword of the
+        // bitmap area (pairs start at even LTs; a lone LT is the chunk's last,
+        // at an even position, in the low half).
+        uint32_t a_bm = st_bm + (PERM ? 4 * rr : 4 * i), a_base = st_base + 4 * rr, a_sd;
+        auto row_at = [&](int k) { return PERM ? a_base + 64 * k : a_bm + 32 * k; };
+        const uint32_t st8 = 8u * st;
         __asm__("v_mov_b32 %0, %1" : "=v"(a_sd) : "s"(st_sd));
         uint32_t a_x[NB];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) a_x[nb] = xq[nb];
         auto decode_one = [&]() {
             const uint32_t mrow = lds_load(row_at(0));
-            const uint32_t base = lds_load(a_base);
             const uint32_t sd = lds_load(a_sd);
-            const i32x4 A = decode_tile<BITS>(lut, mrow, base, sd, lomask, rot);
+            i32x4 A;
+            if constexpr (PERM) A = decode_tile_q(lut, mrow, lds_load(a_bm) & 0xFFFFu, st8, sd, lomask, rot);
+            else A = decode_tile<BITS>(lut, mrow, lds_load(a_base), sd, lomask, rot);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
                 acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, unpack_x(x_pair(a_x[nb])), acc[nb], 0, 0, 0);
                 a_x[nb] += 32;
             }
-            if constexpr (!PERM) a_bm += 32;
+            a_bm += 32;
             a_base += 64;
             a_sd += 4;
         };
         auto decode_two = [&]() {
             const uint32_t m0 = lds_load(row_at(0)), m1 = lds_load(row_at(1));
-            const uint32_t b0 = lds_load(a_base), b1 = lds_load(a_base + 64);
             const uint2 sd = lds_load2(a_sd);
-            const i32x4 A0v = decode_tile<BITS>(lut, m0, b0, sd.x, lomask, rot);
-            const i32x4 A1v = decode_tile<BITS>(lut, m1, b1, sd.y, lomask, rot);
+            i32x4 A0v, A1v;
+            if constexpr (PERM) {
+                const uint32_t w = lds_load(a_bm);
+                A0v = decode_tile_q(lut, m0, w & 0xFFFFu, st8, sd.x, lomask, rot);
+                A1v = decode_tile_q(lut, m1, w >> 16, st8, sd.y, lomask, rot);
+            } else {
+                A0v = decode_tile<BITS>(lut, m0, lds_load(a_base), sd.x, lomask, rot);
+                A1v = decode_tile<BITS>(lut, m1, lds_load(a_base + 64), sd.y, lomask, rot);
+            }
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
                 acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0v, unpack_x(x_pair(a_x[nb])), acc[nb], 0, 0, 0);
                 acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1v, unpack_x(x_pair(a_x[nb] + 32)), acc[nb], 0, 0, 0);
                 a_x[nb] += 64;
             }
-            if constexpr (!PERM) a_bm += 64;
+            a_bm += 64;
             a_base += 128;
             a_sd += 8;
         };
