@@ -38,21 +38,24 @@ HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 1 << 30
 ROUND_LAUNCHES = 200
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_09291_amd", "csrc", f)
-               for f in ("us_spmm_kernel.h", "us_spmm.hip", "us_spmm_narrow.hip", "us_spmm_perm.hip",
-                         "us_spmm_w2.hip")]
+               for f in ("us_spmm_kernel.h", "us_range.h", "us_spmm.hip", "us_spmm_narrow.hip", "us_spmm_perm.hip",
+                         "us_spmm_w2.hip", "us_spmm_burst.h", "us_spmm_burst_plain.hip",
+                         "us_spmm_burst_narrow.hip", "us_spmm_burst_perm.hip", "us_spmm_burst_w2.hip")]
 
 # HBM traffic of one SpMM launch, read from rocprofv3 --pmc runs of this
 # script (one pass for FETCH_SIZE, one for WRITE_SIZE; KiB per dispatch), each
-# divided by what the same counter reads per byte for the plain copy kernel
-# (bench.py --copy-probe 268435456 copies 262144 KiB: FETCH_SIZE reads
-# 131082 KiB and WRITE_SIZE 262144 KiB per dispatch, i.e. 0.50004 and 1.0 KiB
-# per KiB copied). An entry holds only for the kernel sources whose
-# SHA-256 (of the files in KERNEL_SRCS, concatenated) starts with `src`;
-# after any change to them the traffic is unknown. Keyed by workload, N and
-# row reordering.
-COPY_FACTOR = {"FETCH_SIZE": 131082.0 / 262144.0, "WRITE_SIZE": 262144.0 / 262144.0}
+# divided by what the same counter reads per byte copied by a copy kernel of
+# known size. Both copy probes give the same factor: bench.py --copy-probe
+# 268435456 copies 262144 KiB, and FETCH_SIZE reads 131082 KiB per dispatch
+# with plain loads (--copy-kind plain) and 131083 KiB with the SpMM payload's
+# non-temporal buffer loads straight into LDS (--copy-kind lds); WRITE_SIZE
+# reads 262144 KiB for both: 0.50004 and 1.0 KiB per KiB copied. An entry
+# holds only for the kernel sources whose SHA-256 (of the files in
+# KERNEL_SRCS, concatenated) starts with `src`; after any change to them the
+# traffic is unknown. Keyed by workload, N and row reordering.
+COPY_FACTOR = {"FETCH_SIZE": 131083.0 / 262144.0, "WRITE_SIZE": 262144.0 / 262144.0}
 MEASURED_TRAFFIC = {
-    ("ffn_down_4096x11008_s50", 8, False): dict(src="155a1b7dd80d4c75", FETCH_SIZE=11383.46875, WRITE_SIZE=256.0),
+    ("ffn_down_4096x11008_s50", 8, False): dict(src="c5613ae6cb1c534c", FETCH_SIZE=11383.8125, WRITE_SIZE=256.0),
 }
 
 
@@ -92,6 +95,9 @@ def parse():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run the plain copy kernel over BYTES bytes, --steps times (the known "
                          "byte count that calibrates the FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--copy-kind", default="plain", choices=("plain", "lds"),
+                    help="copy probe loads: plain vector loads, or the SpMM payload's non-temporal "
+                         "buffer loads straight into LDS")
     return ap.parse_args()
 
 
@@ -270,12 +276,14 @@ def copy_probe(torch, args, timer):
     nbytes = (args.copy_probe + 15) // 16 * 16
     src = torch.full((nbytes,), 7, dtype=torch.uint8, device="cuda")
     dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
-    ms = timer.run(lambda i: binding.probe_copy(src, dst, nbytes), args.steps)
+    copy = binding.probe_copy_lds if args.copy_kind == "lds" else binding.probe_copy
+    ms = timer.run(lambda i: copy(src, dst, nbytes), args.steps)
     torch.cuda.synchronize()
     if not bool((dst == 7).all()):
         raise RuntimeError("copy probe produced wrong bytes")
     us = ms * 1e3 / args.steps
-    print(json.dumps({"probe": "copy", "bytes_read": nbytes, "bytes_written": nbytes, "steps": args.steps,
+    print(json.dumps({"probe": "copy", "kind": args.copy_kind, "bytes_read": nbytes, "bytes_written": nbytes,
+                      "steps": args.steps,
                       "us_per_call": round(us, 3), "gbs": round(2 * nbytes / (us * 1e-6) / 1e9, 1)}),
           flush=True)
 

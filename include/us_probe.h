@@ -43,6 +43,12 @@ size_t us_probe_read_sink_words(size_t bytes);
 /* dst[0 .. bytes) = src[0 .. bytes); both 16-byte aligned, bytes % 16 == 0. */
 us_status us_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
 
+/* The same copy, reading `src` with the loads the SpMM kernels stage their
+ * payload with (non-temporal 16-byte buffer loads straight into LDS), then
+ * storing from LDS; bytes at most 2 GiB. It calibrates HBM read counters for
+ * that kind of load. US_ERR_ARG as us_probe_copy, or for a larger size. */
+us_status us_probe_copy_lds(const void *src, void *dst, size_t bytes, void *stream);
+
 /* One wavefront spins until `ns` nanoseconds of the GPU's constant-rate clock
  * have passed (at most one second), then exits. */
 us_status us_probe_spin(uint64_t ns, void *stream);

@@ -27,7 +27,7 @@ K_MAX = 130048
 #: Every symbol the two public headers declare.
 EXPORTS = ("us_encode", "us_encode_w2", "us_encode_reordered", "us_iebme_free", "us_pmr", "us_pmr_formats", "us_spmm_plan", "us_spmm_workspace_size", "us_spmm", "us_spmm_noalloc",
            "us_gemm_i8", "us_status_string", "us_probe_read", "us_probe_read_sink_words",
-           "us_probe_copy", "us_probe_spin")
+           "us_probe_copy", "us_probe_copy_lds", "us_probe_spin")
 
 
 class UsError(RuntimeError):
@@ -116,9 +116,10 @@ def lib():
         L.us_probe_read_sink_words.argtypes = [sz]
         L.us_probe_read_sink_words.restype = sz
         L.us_probe_copy.argtypes = [vp, vp, sz, vp]
+        L.us_probe_copy_lds.argtypes = [vp, vp, sz, vp]
         L.us_probe_spin.argtypes = [ctypes.c_uint64, vp]
         for name in ("us_encode", "us_encode_w2", "us_encode_reordered", "us_pmr", "us_pmr_formats", "us_spmm_workspace_size", "us_spmm_plan", "us_spmm", "us_spmm_noalloc", "us_gemm_i8",
-                     "us_probe_read", "us_probe_copy", "us_probe_spin"):
+                     "us_probe_read", "us_probe_copy", "us_probe_copy_lds", "us_probe_spin"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -343,6 +344,12 @@ def probe_read_sink_words(nbytes: int) -> int:
 def probe_copy(src, dst, nbytes: int, stream=None) -> None:
     _check("us_probe_copy", lib().us_probe_copy(src.data_ptr(), dst.data_ptr(), nbytes,
                                                 _stream_handle(stream)))
+
+
+def probe_copy_lds(src, dst, nbytes: int, stream=None) -> None:
+    """us_probe_copy_lds: the copy with non-temporal buffer loads straight into LDS."""
+    _check("us_probe_copy_lds", lib().us_probe_copy_lds(src.data_ptr(), dst.data_ptr(), nbytes,
+                                                        _stream_handle(stream)))
 
 
 def probe_spin(ns: int, stream=None) -> None:

@@ -165,6 +165,41 @@ __global__ __launch_bounds__(kProbeThreads) void probe_copy_kernel(const i32x4 *
         dst[idx] = src[idx];
 }
 
+// The same copy with the loads the SpMM kernels stage their payload with:
+// non-temporal buffer_load_dwordx4 straight into LDS, 1 KB per wavefront
+// and step (lane l's 16 bytes at LDS base + 16 l, the base in M0); each lane
+// then reads its 16 bytes back from LDS and stores them to dst. Bytes past
+// the buffer's range read as zero and are not stored. The LDS read of one
+// step is complete (its value feeds the store) before the next step's load
+// overwrites the buffer.
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
+typedef __attribute__((address_space(3))) i32x4 lds_i32x4;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void probe_dma16_nt(u32x4 desc, uint32_t lds, uint32_t voff) {
+    __asm__ volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds\n\ts_waitcnt vmcnt(0)"
+                     :
+                     : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(desc)
+                     : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+__global__ __launch_bounds__(kProbeThreads) void probe_copy_lds_kernel(const uint8_t *__restrict__ src,
+                                                                       i32x4 *__restrict__ dst, uint32_t n16) {
+    __shared__ __attribute__((aligned(16))) uint32_t buf[kProbeThreads * 4];
+    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint32_t lds = (uint32_t)(size_t)(lds_u32 *)buf + 1024u * wave;
+    const uint64_t sa = (uint64_t)(size_t)src;
+    const u32x4 desc = (u32x4){(uint32_t)sa, (uint32_t)(sa >> 32) & 0xFFFFu, 16u * n16, 0x00020000u};
+    const uint32_t waves = gridDim.x * (kProbeThreads / 64);
+    for (uint32_t piece = blockIdx.x * (kProbeThreads / 64) + wave; 64ull * piece < n16; piece += waves) {
+        probe_dma16_nt(desc, lds, 1024u * piece + 16u * lane);
+        const i32x4 v = *(const lds_i32x4 *)(size_t)(lds + 16u * lane);
+        if (64u * piece + lane < n16) dst[64u * piece + lane] = v;
+    }
+}
+
 __global__ void probe_spin_kernel(uint64_t ticks) {
     const uint64_t t0 = wall_clock64();
     while (wall_clock64() - t0 < ticks) __builtin_amdgcn_s_sleep(8);
@@ -224,6 +259,15 @@ extern "C" us_status us_probe_copy(const void *src, void *dst, size_t bytes, voi
     const size_t n16 = bytes / 16;
     hipLaunchKernelGGL(probe_copy_kernel, dim3((unsigned)probe_blocks(n16)), dim3(kProbeThreads), 0,
                        (hipStream_t)stream, (const i32x4 *)src, (i32x4 *)dst, n16);
+    return hipGetLastError() == hipSuccess ? US_OK : US_ERR_DEVICE;
+}
+
+extern "C" us_status us_probe_copy_lds(const void *src, void *dst, size_t bytes, void *stream) {
+    if (!src || !dst || bytes == 0 || bytes % 16 || !aligned16(src) || !aligned16(dst)) return US_ERR_ARG;
+    if (bytes > ((size_t)1 << 31)) return US_ERR_ARG;
+    const size_t n16 = bytes / 16;
+    hipLaunchKernelGGL(probe_copy_lds_kernel, dim3((unsigned)probe_blocks(n16)), dim3(kProbeThreads), 0,
+                       (hipStream_t)stream, (const uint8_t *)src, (i32x4 *)dst, (uint32_t)n16);
     return hipGetLastError() == hipSuccess ? US_OK : US_ERR_DEVICE;
 }
 

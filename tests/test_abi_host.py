@@ -265,6 +265,8 @@ def test_probe_argument_errors():
     assert L.us_probe_read(0x10, 16, 0x10, -1, None) == -1
     assert L.us_probe_read(0x10, 16, 0x10, binding.PROBE_READ_SHAPES, None) == -1
     assert L.us_probe_copy(0x10, 0x18, 16, None) == -1
+    assert L.us_probe_copy_lds(0x10, 0x18, 16, None) == -1
+    assert L.us_probe_copy_lds(0x10, 0x20, (1 << 31) + 16, None) == -1
     assert L.us_probe_spin(2 * 10 ** 9, None) == -1
 
 

@@ -58,6 +58,13 @@ def test_probe_read_and_copy(torch_cuda):
     binding.probe_copy(src, dst, n)
     torch.cuda.synchronize()
     assert np.array_equal(dst.cpu().numpy(), host)
+    # Through LDS, also with a ragged tail (not a whole 1 KB step).
+    for m in (n, n - 16 * 37):
+        dst = torch.zeros(n, dtype=torch.uint8, device="cuda")
+        binding.probe_copy_lds(src, dst, m)
+        torch.cuda.synchronize()
+        got = dst.cpu().numpy()
+        assert np.array_equal(got[:m], host[:m]) and not got[m:].any(), m
 
 
 def test_probe_spin_returns(torch_cuda):

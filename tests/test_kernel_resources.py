@@ -21,7 +21,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2608_09291_amd", "csrc")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-UNITS = ("us_spmm", "us_spmm_narrow", "us_spmm_perm", "us_spmm_w2", "us_spmm_burst_plain", "us_spmm_burst_narrow",
+UNITS = ("us_dense", "us_spmm", "us_spmm_narrow", "us_spmm_perm", "us_spmm_w2", "us_spmm_burst_plain", "us_spmm_burst_narrow",
          "us_spmm_burst_perm", "us_spmm_burst_w2")
 FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fno-strict-aliasing", "-Xclang", "-target-feature",
          "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"), "-I", CSRC, "--cuda-device-only", "-S"]
@@ -96,8 +96,9 @@ def burst_waves_per_simd(wpg, nmax):
 
 
 def test_m0_is_only_the_direct_payload_loads(kernels):
-    # The direct-to-LDS loads set M0 in assembly and list it as clobbered;
-    # that is only sound while the compiler itself keeps nothing in M0. The
+    # The direct-to-LDS loads (the SpMM kernels' and the copy probe's) set
+    # M0 in assembly and list it as clobbered; that is only sound while the
+    # compiler itself keeps nothing in M0. The
     # LDS base must come from a scalar register: a vector register there
     # (a value the compiler did not prove wave-uniform) would not be a valid
     # M0 source, so every write is checked to name an SGPR.
