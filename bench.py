@@ -88,6 +88,12 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(synth.WORKLOADS))
     ap.add_argument("--N", type=int, default=0, help="activation columns (default: the workload's first)")
     ap.add_argument("--split-k", type=int, default=0)
+    ap.add_argument("--variant", type=int, default=0, choices=(0, 1, 2, 3),
+                    help="us_spmm_opts.variant: 0 automatic, 1 whole / 2 ring staging, 3 single pass "
+                         "(needs --split-k)")
+    ap.add_argument("--chunk-lts", type=int, default=0, help="us_spmm_opts.chunk_lts (0: automatic)")
+    ap.add_argument("--k-blocks", type=int, default=0,
+                    help="us_spmm_opts.k_blocks: workgroups per row block with the single pass (0: one)")
     ap.add_argument("--reorder", action="store_true", help="row-reorder the LTs before encoding")
     ap.add_argument("--bits", type=int, default=4, choices=(4, 2), help="weight bits (4: W4A4, 2: W2A4)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -168,8 +174,13 @@ def spmm_bench(torch, args, w, N, timer, reorder=False, bits=4):
     L = binding.lib()
     structs = [c.struct() for c in copies]
     sptrs = [ctypes.byref(s) for s in structs]
-    opts = binding.SpmmOpts(args.split_k, 0)
+    opts = binding.SpmmOpts(args.split_k, args.variant, args.chunk_lts, args.k_blocks)
     optp = ctypes.byref(opts)
+    # A split across workgroups takes a zeroed reduction workspace, which
+    # every call leaves zeroed again.
+    ws_bytes = binding.workspace_size(w.M, w.K, N, args.split_k, args.variant, args.chunk_lts, args.k_blocks)
+    ws = torch.zeros(max(1, ws_bytes // 4), dtype=torch.int32, device="cuda") if ws_bytes else None
+    wsa = None if ws is None else ws.data_ptr()
     xa, ya = xp.data_ptr(), y.data_ptr()
     sca = None if sc is None else sc.data_ptr()
     yfa = None if yf is None else yf.data_ptr()
@@ -177,7 +188,7 @@ def spmm_bench(torch, args, w, N, timer, reorder=False, bits=4):
     status = [0]
 
     def launch(i):
-        st = L.us_spmm(sptrs[i % n_copies], xa, N, ya, sca, yfa, None, 0, optp, sh)
+        st = L.us_spmm(sptrs[i % n_copies], xa, N, ya, sca, yfa, wsa, ws_bytes, optp, sh)
         if st:
             status[0] = st
 
@@ -338,7 +349,8 @@ def main():
         log(f"[bench] cpu oracle {cpu['ms_per_call']} ms/call on {cpu['cores']} threads")
 
     rep = r["rep"]
-    plan = binding.spmm_plan(w.M, w.K, N, args.split_k, reordered=args.reorder, bits=args.bits)
+    plan = binding.spmm_plan(w.M, w.K, N, args.split_k, args.variant, reordered=args.reorder, bits=args.bits,
+                             chunk_lts=args.chunk_lts, k_blocks=args.k_blocks, full=True)
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -354,8 +366,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "M": w.M, "K": w.K, "N": N, "sparsity": w.sparsity,
                    "dequant": w.dequant, "weight_bits": args.bits, "reordered": args.reorder,
-                   "split_k": plan[0], "chunk_lts": plan[1],
-                   "staging": "ring" if plan[2] == 2 else "whole", "plan": "auto" if not args.split_k else "forced",
+                   "split_k": plan[0], "chunk_lts": plan[1], "k_blocks": plan[3],
+                   "staging": {1: "whole", 2: "ring", 3: "single pass"}[plan[2]],
+                   "plan": "auto" if not (args.split_k or args.variant or args.chunk_lts or args.k_blocks) else "forced",
                    "weights": f"w{args.bits}a4 IE-BME (16x64 tiles, 2x2 areas), int8 MFMA, int32 accumulate",
                    "rotating_copies": r["n_copies"]},
         "us_per_call": round(us, 3),
@@ -369,7 +382,9 @@ def main():
         "ci_eff_eq2": round(rep["ci_eff"], 3),
         "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(w.name, N, args.reorder) if args.bits == 4 else None,
+                     "traffic": (measured_traffic(w.name, N, args.reorder)
+                                 if args.bits == 4 and not (args.split_k or args.variant or args.chunk_lts
+                                                            or args.k_blocks) else None),
                      "kernel": "us_spmm_kernel",
                      "bytes_per_launch": r["alg_bytes"]},
         "cpu_baseline": cpu,
