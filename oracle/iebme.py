@@ -24,6 +24,14 @@ Readings taken where the paper is silent:
     b = 2 (the W2A4 setting of the evaluation) the payload packs four values
     per byte, value n at bits 2 (n mod 4) .. 2 (n mod 4) + 1 of byte n // 4,
     everything else (mask, offsets in values, stream order) unchanged.
+
+Value order within an LT. The storage-layout passage puts area q's value at
+rank rho at CV[o_t + q P_t + rho] (``order="areas"``, the paper's order).
+The library stores the same values in a second order (``order="area_rows"``):
+the C_A areas of one area row alternate value by value, area (a, c) at rank
+rho at CV[o_t + a C_A P_t + C_A rho + c], so that one read at a rank serves
+every area of the row. Offsets, bitmaps, P_t and the byte count are the same
+in both orders; only the positions of the values inside an LT differ.
 """
 from __future__ import annotations
 
@@ -59,6 +67,7 @@ class Encoded:
     P: np.ndarray         # int64 per LT: P_t = ||B_t||_0
     nnz: int
     bits: int = 4         # bits per payload value
+    order: str = "areas"  # value order within an LT (see the module docstring)
 
     @property
     def Q(self) -> int:
@@ -109,8 +118,29 @@ def areas(T: np.ndarray, ra: int, ca: int) -> np.ndarray:
     return T.reshape(n_lt, ra, hb, ca, kb).transpose(0, 1, 3, 2, 4).reshape(n_lt, ra * ca, hb, kb)
 
 
-def encode(W, lt_h: int = 16, lt_w: int = 64, ra: int = 2, ca: int = 2, bits: int = 4) -> Encoded:
+VALUE_ORDERS = ("areas", "area_rows")
+
+
+def value_address(off, P, q, rho, ca: int, order: str):
+    """Position in the compressed-values array of area q's value at rank rho
+    of an LT with offset off and P active union-mask entries.
+
+    "areas": o_t + q P_t + rho (the storage-layout passage of Section V-A);
+    "area_rows": area q = a C_A + c at o_t + a C_A P_t + C_A rho + c.
+    """
+    if order == "areas":
+        return off + q * P + rho
+    if order == "area_rows":
+        a, c = q // ca, q % ca
+        return off + a * ca * P + ca * rho + c
+    raise ValueError(f"unknown value order {order!r}")
+
+
+def encode(W, lt_h: int = 16, lt_w: int = 64, ra: int = 2, ca: int = 2, bits: int = 4,
+           order: str = "areas") -> Encoded:
     """IE-BME encoding of a masked b-bit matrix (Section V-A)."""
+    if order not in VALUE_ORDERS:
+        raise ValueError(f"unknown value order {order!r}")
     W = check_weights(W, bits)
     M, K = W.shape
     if M % lt_h or K % lt_w or lt_h % ra or lt_w % ca:
@@ -144,19 +174,19 @@ def encode(W, lt_h: int = 16, lt_w: int = 64, ra: int = 2, ca: int = 2, bits: in
     bitmaps = words.reshape(-1).astype(np.uint64)
 
     # Compressed Values: compact rank rho_t(i, j) = active entries before (i, j)
-    # in row-major order; CV[o_t + q * P_t + rho] = W_t^(q)(i, j).
+    # in row-major order; CV[o_t + q * P_t + rho] = W_t^(q)(i, j) in the
+    # paper's order, or at value_address(...) in the chosen order.
     flat = B.reshape(n_lt, nbits)
     rho = np.cumsum(flat, axis=1) - flat
     t_idx, pos = np.nonzero(flat)
     vals = A.reshape(n_lt, Q, nbits)[t_idx, :, pos]                       # (n_active, Q)
-    addr = (offsets[t_idx][:, None]
-            + np.arange(Q, dtype=np.int64)[None, :] * P[t_idx][:, None]
-            + rho[t_idx, pos][:, None])
+    addr = value_address(offsets[t_idx][:, None], P[t_idx][:, None], np.arange(Q, dtype=np.int64)[None, :],
+                         rho[t_idx, pos][:, None], ca, order)
     cv = np.zeros(int(offsets[-1]), dtype=np.int64)
     cv[addr.ravel()] = vals.ravel()
 
     return Encoded(M, K, lt_h, lt_w, ra, ca, bitmaps, offsets.astype(np.uint32),
-                   pack_values(cv, bits), P, int(np.count_nonzero(W)), bits)
+                   pack_values(cv, bits), P, int(np.count_nonzero(W)), bits, order)
 
 
 def pack_values(v: np.ndarray, bits: int) -> np.ndarray:
@@ -227,8 +257,9 @@ def union_mask(enc: Encoded) -> np.ndarray:
 def decode(enc: Encoded) -> np.ndarray:
     """Inverse of encode: rebuild the dense INT4 matrix from the three arrays.
 
-    Every active (i, j) of LT t takes W_t^(q)(i, j) = CV[o_t + q * P_t + rho_t(i, j)];
-    every inactive position is zero in all Q areas.
+    Every active (i, j) of LT t takes W_t^(q)(i, j) = CV[o_t + q * P_t + rho_t(i, j)]
+    (or the value at value_address in the encoding's order); every inactive
+    position is zero in all Q areas.
     """
     hb, kb = enc.area_shape
     Q, n_lt = enc.Q, enc.n_lt
@@ -241,8 +272,8 @@ def decode(enc: Encoded) -> np.ndarray:
     rho = np.cumsum(B, axis=1) - B
     A = np.zeros((n_lt, Q, hb * kb), dtype=np.int64)
     t_idx, pos = np.nonzero(B)
-    addr = (off[t_idx][:, None] + np.arange(Q, dtype=np.int64)[None, :] * P[t_idx][:, None]
-            + rho[t_idx, pos][:, None])
+    addr = value_address(off[t_idx][:, None], P[t_idx][:, None], np.arange(Q, dtype=np.int64)[None, :],
+                         rho[t_idx, pos][:, None], enc.ca, enc.order)
     A[t_idx, :, pos] = cv[addr]
     # Undo the area partitioning, then the LT tiling.
     T = (A.reshape(n_lt, enc.ra, enc.ca, hb, kb).transpose(0, 1, 3, 2, 4)
@@ -290,7 +321,8 @@ def lspd_decode_tile(enc: Encoded, t: int, G: int) -> np.ndarray:
     Pt = int(Bt.sum())
     o = int(enc.offsets[t])
     cv = unpack_values(enc.payload, int(enc.offsets[-1]), enc.bits)
-    streams = [cv[o + q * Pt: o + (q + 1) * Pt] for q in range(enc.Q)]
+    rhos = np.arange(Pt, dtype=np.int64)
+    streams = [cv[value_address(o, Pt, q, rhos, enc.ca, enc.order)] for q in range(enc.Q)]
     A = np.zeros((enc.Q, hb, kb), dtype=np.int64)
     for r in range(hb):
         for g in range(kb // G):
