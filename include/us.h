@@ -59,14 +59,18 @@ typedef enum {
  * any area is nonzero at (i, j); it is bit (32 i + j) % 64 of word
  * 4 t + (32 i + j) / 64 of `bitmaps`. offsets[t] = sum over tau < t of 4 P_tau
  * (P = active union-mask bits), in INT4 values, with offsets[n_lt] the total.
- * Payload value o_t + q P_t + rho (rho = rank of (i, j) among active bits,
- * row-major) is area q's value at (i, j); value n is the low nibble of byte
- * n / 2 when n is even, the high nibble when odd, in two's complement.
+ * Payload: area q = 2 a + c's value at (i, j), for every active (i, j) of
+ * rank rho (its place among the LT's active bits, row-major), is value
+ * o_t + 4 a P_t + 2 rho + c: the two areas of an area row alternate by rank,
+ * so one read at a rank fetches both. (The paper lists each area's values in
+ * turn, o_t + q P_t + rho; the values of an LT, the offsets and the byte
+ * count are the same.) Value n is the low nibble of byte n / 2 when n is
+ * even, the high nibble when odd, in two's complement.
  *
  * With bits = 2 (W2A4, us_encode_w2) the weights are signed 2-bit values in
  * [-2, 1] and payload value n sits at bits 2 (n mod 4) .. 2 (n mod 4) + 1 of
  * byte n / 4; the bitmaps, the offsets (still counted in values) and the
- * stream order are those of the 4-bit format.
+ * value order are those of the 4-bit format.
  *
  * Row reordering (Section V-B) is recorded in `perm`. When it is NULL the
  * LTs keep their row order. Otherwise bits 4p .. 4p + 3 of perm[t] hold

@@ -160,11 +160,12 @@ def perm_words(perms) -> np.ndarray:
     return np.bitwise_or.reduce(perms << shifts, axis=1).astype(np.uint64)
 
 
-def encode_reordered(W, lt_h: int = 16, lt_w: int = 64, ra: int = 2, ca: int = 2):
-    """Row reordering (Section V-B) followed by IE-BME (Section V-A).
+def encode_reordered(W, lt_h: int = 16, lt_w: int = 64, ra: int = 2, ca: int = 2, order: str = "areas"):
+    """Row reordering (Section V-B) followed by IE-BME (Section V-A), with the
+    values of each LT in ``order`` (see oracle.iebme).
 
     Returns (Encoded of the reordered matrix, perms).
     """
     Wr, perms, _ = reorder(W, lt_h, lt_w, ra, ca)
-    enc: Encoded = encode(Wr, lt_h, lt_w, ra, ca)
+    enc: Encoded = encode(Wr, lt_h, lt_w, ra, ca, order=order)
     return enc, perms

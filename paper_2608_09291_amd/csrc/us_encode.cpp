@@ -268,9 +268,13 @@ us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool r
         return US_ERR_NOMEM;
     }
 
-    // Pass 2: Compressed Values, CV[o_t + q P_t + rho] = W_t^(q)(i, j) for
-    // every active (i, j), zeros of active groups included; value n takes
-    // bits (n mod per_byte) * bits of byte n / per_byte. Each LT starts on a
+    // Pass 2: Compressed Values: area q = a C_A + c's value at (i, j), zeros
+    // of active groups included, for every active (i, j) of rank rho. The
+    // areas of one area row alternate by rank (value o_t + a C_A P_t +
+    // C_A rho + c), so the C_A values a rank selects in an area row sit
+    // together; the paper lists each area's values in turn (o_t + q P_t +
+    // rho), which holds the same values per LT. Value n takes bits
+    // (n mod per_byte) * bits of byte n / per_byte. Each LT starts on a
     // multiple of four values, so LTs never share a byte.
     parallel_ranges(n_lt, [&](int64_t t0, int64_t t1) {
         for (int64_t t = t0; t < t1; ++t) {
@@ -284,7 +288,7 @@ us_status encode_impl(const int8_t *w, int32_t M, int32_t K, int64_t ldw, bool r
                 if (!((bm[L >> 6] >> (L & 63)) & 1)) continue;
                 const int i = L / kAreaW, j = L % kAreaW;
                 for (int q = 0; q < US_RA * US_CA; ++q) {
-                    const uint64_t n = o + (uint64_t)q * Pt + rho;
+                    const uint64_t n = o + (uint64_t)(q / US_CA) * US_CA * Pt + (uint64_t)US_CA * rho + (q % US_CA);
                     const uint8_t v = (uint8_t)area_value(rows, q, i, j) & (uint8_t)((1 << bits) - 1);
                     payload[n / per_byte] |= (uint8_t)(v << ((n % per_byte) * bits));
                 }

@@ -43,11 +43,11 @@ namespace us_spmm_detail {
 //   payload : the slice's compressed values from the 16-byte boundary at or
 //             below its first byte; 8 BITS CH + 2 pieces of 16 bytes cover
 //             the largest slice (an LT holds at most 1024 values) with the
-//             8-byte overhang of its last window;
+//             12-byte overhang of its last window;
 //   bitmaps : union-mask rows, 8 dwords per LT;
-//   records : without PERM the row base of each lane row (16 dwords per LT);
-//             with PERM [row base, mask row] per lane row (32 dwords per LT);
-//   sd      : per LT, the bits of one area stream, BITS (o_{t+1} - o_t) / 4;
+//   records : without PERM the row base (a slot address, see the chunked
+//             kernel) of each lane row (16 dwords per LT); with PERM
+//             [row base, mask row] per lane row (32 dwords per LT);
 //   offsets : o_t of the slice's LTs and the end offset;
 //   perm    : (PERM) the row permutation word of each LT;
 //   X       : the slice's activations, one row of 32 bytes per LT for each
@@ -63,8 +63,7 @@ struct Burst {
     static constexpr int kRec = PERM ? 128 : 64;              // record bytes per LT
     static constexpr int kBmOffset = 16 * kPayPieces;
     static constexpr int kRecOffset = kBmOffset + 32 * kLtPad;
-    static constexpr int kSdOffset = kRecOffset + kRec * kLtPad;
-    static constexpr int kOffOffset = kSdOffset + 4 * kLtPad;
+    static constexpr int kOffOffset = kRecOffset + kRec * kLtPad;
     static constexpr int kPermOffset = (kOffOffset + 4 * (kLtPad + 1) + 7) & ~7;
     static constexpr int kXOffset = (kPermOffset + (PERM ? 8 * kLtPad : 0) + 15) & ~15;
     static constexpr int kXRowWords = 8 * CH + 4;
@@ -104,23 +103,6 @@ __device__ __forceinline__ void dma16_keep(u32x4 desc, uint32_t lds, uint32_t vo
                      : "memory", "m0");
 }
 #pragma clang diagnostic pop
-
-// The data half of decode_tile: the two windows (8-byte LDS reads at the
-// dwords holding bit addresses bn0 and bn1) placed by the selector pair.
-template <int BITS>
-__device__ __forceinline__ i32x4 place_tile(uint2 d0, uint2 d1, uint32_t bn0, uint32_t bn1, u32x2 sv) {
-    const uint32_t w0 = __builtin_amdgcn_alignbit(d0.y, d0.x, bn0), w1 = __builtin_amdgcn_alignbit(d1.y, d1.x, bn1);
-    const uint2 sel = make_uint2(sv.x, sv.y);
-    int2 c0, c1;
-    if constexpr (BITS == 4) {
-        c0 = place(w0, sel);
-        c1 = place(w1, sel);
-    } else {
-        c0 = place2(w0, sel);
-        c1 = place2(w1, sel);
-    }
-    return (i32x4){c0.x, c0.y, c1.x, c1.y};
-}
 
 // Eight INT4 activations of each of two dwords -> the four B-operand dwords,
 // values in the high nibble (16 x), slot order of unpack_x.
@@ -180,7 +162,7 @@ __global__ __launch_bounds__(64 * WPG, burst_waves_per_simd(WPG, NMAX)) void us_
 
     const uint32_t st = lds0 + (uint32_t)(wave * stage_bytes);
     const uint32_t st_bm = st + C::kBmOffset, st_rec = st + C::kRecOffset;
-    const uint32_t st_sd = st + C::kSdOffset, st_off = st + C::kOffOffset;
+    const uint32_t st_off = st + C::kOffOffset;
     const uint32_t st_pm = st + C::kPermOffset, st_x = st + C::kXOffset;
 
     // Inputs, straight into the stage with direct-to-LDS loads, each lane
@@ -272,12 +254,13 @@ __global__ __launch_bounds__(64 * WPG, burst_waves_per_simd(WPG, NMAX)) void us_
             const uint2 o = lds_load2(st_off + 4 * min(j, (uint32_t)CH - 1));
             [[maybe_unused]] uint32_t pm = 0;
             if constexpr (PERM) pm = lds_load(st_pm + 8 * j + 4 * (rr & 1));
-            const uint32_t inj = amask & ((o.y - o.x) >> 1);
+            const uint32_t inj = amask & ((o.y - o.x) >> 2);      // P_t
             uint32_t ex = (uint32_t)__builtin_amdgcn_update_dpp((int)inj, (int)__popc(mrow), 0x112, 0xF, 0xF, false);
             ex += dpp_row<0x112>(ex);
             ex += dpp_row<0x114>(ex);
             ex += dpp_row<0x118>(ex);
-            const uint32_t bval = 8u * st + ((uint32_t)BITS * (o.x + ex) - 8u * A0);
+            constexpr uint32_t kSlotsPerByte = 4 / BITS;
+            const uint32_t bval = kSlotsPerByte * st + ((o.x >> 1) + ex - kSlotsPerByte * A0);
             if constexpr (PERM) {
                 const uint32_t rec = st_rec + C::kRec * j;
                 lds_store2(rec + 8 * rr, (u32x2){bval, mrow});
@@ -286,15 +269,12 @@ __global__ __launch_bounds__(64 * WPG, burst_waves_per_simd(WPG, NMAX)) void us_
             } else {
                 lds_store(st_rec + C::kRec * j + 4 * rr, bval);
             }
-            if (rr == 0) lds_store(st_sd + 4 * j, ((o.y - o.x) * (uint32_t)BITS) >> 2);
         }
     }
 
     // Decode, pair by pair, in a fixed order.
     const uint32_t a_bm = st_bm + 4 * i;
     const uint32_t a_rec = st_rec + (PERM ? 8 : 4) * rr;
-    uint32_t a_sd;
-    __asm__("v_mov_b32 %0, %1" : "=v"(a_sd) : "s"(st_sd));
     uint32_t a_x = st_x + 4u * (uint32_t)(min(rr, N - 1) * C::kXRowWords + g);
     __asm__("" : "+v"(a_x));                               // one base register, immediate offsets per LT
     i32x4 acc = (i32x4){0, 0, 0, 0};
@@ -315,44 +295,44 @@ __global__ __launch_bounds__(64 * WPG, burst_waves_per_simd(WPG, NMAX)) void us_
         constexpr int j = decltype(jc)::value;
         return make_uint2(lds_load(a_x + 32 * j), lds_load(a_x + 32 * j + 16));
     };
-    auto decode_one = [&](auto jc, uint32_t sd) {
+    auto decode_one = [&](auto jc) {
         uint32_t mrow, base;
         row_of(jc, mrow, base);
-        const i32x4 A = decode_tile<BITS>(lut, mrow, base, sd, lomask, rot);
+        const i32x4 A = decode_tile<BITS>(lut, mrow, base, lomask, rot);
         acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, unpack_x2(x_of(jc)), acc, 0, 0, 0);
     };
     // Two LTs with every LDS request of both issued before either waits:
     // addresses of both, then the windows, selectors and activations of both,
     // then the placement of both.
-    auto decode_two = [&](auto jc, uint2 sd) {
+    auto decode_two = [&](auto jc) {
         constexpr int j = decltype(jc)::value;
         uint32_t m0, b0, m1, b1;
         row_of(std::integral_constant<int, j>(), m0, b0);
         row_of(std::integral_constant<int, j + 1>(), m1, b1);
-        const uint32_t p0 = b0 + (uint32_t)BITS * __popc(m0 & lomask), q0 = p0 + sd.x;
-        const uint32_t p1 = b1 + (uint32_t)BITS * __popc(m1 & lomask), q1 = p1 + sd.y;
-        const uint32_t s0 = __builtin_amdgcn_alignbit(m0, m0, rot) & 0x7F8u;
-        const uint32_t s1 = __builtin_amdgcn_alignbit(m1, m1, rot) & 0x7F8u;
-        const uint2 w0 = lds_load2((p0 >> 3) & ~3u), v0 = lds_load2((q0 >> 3) & ~3u);
-        const uint2 w1 = lds_load2((p1 >> 3) & ~3u), v1 = lds_load2((q1 >> 3) & ~3u);
-        const u32x2 e0 = *(const u32x2 *)((const char *)lut + s0);
-        const u32x2 e1 = *(const u32x2 *)((const char *)lut + s1);
+        const uint32_t p0 = b0 + (uint32_t)__popc(m0 & lomask);
+        const uint32_t p1 = b1 + (uint32_t)__popc(m1 & lomask);
+        const SlotWin<BITS> w0 = slot_window<BITS>(p0), w1 = slot_window<BITS>(p1);
+        const uint2 e0 = selectors(lut, m0, rot), e1 = selectors(lut, m1, rot);
         const uint2 x0 = x_of(std::integral_constant<int, j>()), x1 = x_of(std::integral_constant<int, j + 1>());
-        const i32x4 A0v = place_tile<BITS>(w0, v0, p0, q0, e0);
-        const i32x4 A1v = place_tile<BITS>(w1, v1, p1, q1, e1);
+        const i32x4 A0v = place_slots<BITS>(w0, p0, e0);
+        const i32x4 A1v = place_slots<BITS>(w1, p1, e1);
         acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0v, unpack_x2(x0), acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1v, unpack_x2(x1), acc, 0, 0, 0);
     };
     // A pair whose second LT exists takes a straight-line path of its own.
     // Pair p covers LTs 2p and 2p + 1: at most 128 BITS (2p + 2) + 15 bytes
-    // from A0 with the alignment, plus the 8-byte window overhang, so it
-    // needs loads up to U(p) = min(kLoads - 1, (256 BITS (p + 1) + 23) / 1024).
+    // from A0 with the alignment, plus the window overhang (12 bytes for
+    // 4-bit slots, 8 for 2-bit), so it needs loads up to
+    // U(p) = min(kLoads - 1, (256 BITS (p + 1) + 15 + overhang) / 1024).
+    constexpr int kSpan = BITS == 4 ? 27 : 23;
     static_for<0, (CH + 1) / 2>([&](auto pc) {
         constexpr int pr = decltype(pc)::value;
-        constexpr int kNeed = (256 * BITS * (pr + 1) + 23) / 1024 < C::kLoads - 1 ? (256 * BITS * (pr + 1) + 23) / 1024
-                                                                                 : C::kLoads - 1;
-        constexpr int kPrev = pr == 0 ? -1 : ((256 * BITS * pr + 23) / 1024 < C::kLoads - 1 ? (256 * BITS * pr + 23) / 1024
-                                                                                            : C::kLoads - 1);
+        constexpr int kNeed = (256 * BITS * (pr + 1) + kSpan) / 1024 < C::kLoads - 1
+                                  ? (256 * BITS * (pr + 1) + kSpan) / 1024
+                                  : C::kLoads - 1;
+        constexpr int kPrev = pr == 0 ? -1
+                              : ((256 * BITS * pr + kSpan) / 1024 < C::kLoads - 1 ? (256 * BITS * pr + kSpan) / 1024
+                                                                                  : C::kLoads - 1);
         if (2 * pr < nlt) {
             // Loads issued so far: those up to kPrev + WIN (or the first WIN).
             constexpr int kIssued = (kPrev + 1 + WIN) < C::kLoads ? kPrev + 1 + WIN : C::kLoads;
@@ -363,12 +343,12 @@ __global__ __launch_bounds__(64 * WPG, burst_waves_per_simd(WPG, NMAX)) void us_
             __asm__ volatile("" ::: "memory");
             if constexpr (2 * pr + 1 < CH) {
                 if (2 * pr + 1 < nlt) {
-                    decode_two(std::integral_constant<int, 2 * pr>(), lds_load2(a_sd + 8 * pr));
+                    decode_two(std::integral_constant<int, 2 * pr>());
                 } else {
-                    decode_one(std::integral_constant<int, 2 * pr>(), lds_load(a_sd + 8 * pr));
+                    decode_one(std::integral_constant<int, 2 * pr>());
                 }
             } else {
-                decode_one(std::integral_constant<int, 2 * pr>(), lds_load(a_sd + 8 * pr));
+                decode_one(std::integral_constant<int, 2 * pr>());
             }
         }
     });

@@ -33,17 +33,18 @@
 //    one wavefront straight into the A operand of v_mfma_i32_16x16x64_i8.
 //    Lane l owns MFMA row l % 16 = 2 i + a (union-mask row i, area row a) and
 //    k-group g = l / 16, which is the G = 8 bit segment g of mask row i.
-//    idx_base is split in two: the popcount of the rows before row i (plus
-//    2 P_t for area row a = 1, whose streams start two streams later) is the
+//    idx_base is split in two: the popcount of the rows before row i is the
 //    same for all four segments of a row, so it is computed once per LT and
-//    chunk by a DPP scan over 16 lanes and kept in LDS as a stage bit address;
-//    each lane adds the popcount of its row below bit 8 g. The same index then
-//    reads area stream q = 2a (columns 8g..8g+7) and stream q = 2a + 1
-//    (columns 32+8g..32+8g+7): as in the paper, one rank serves every area
-//    stream. Active nibbles are placed into their byte slots with two
-//    v_perm_b32 per 8 positions, selectors taken from a 256-entry table
-//    indexed by the 8-bit segment; inactive slots get selector 0x0C (zero).
-//    LTs are decoded in pairs so that two independent chains interleave.
+//    chunk by a DPP scan over 16 lanes and kept in LDS as a stage slot
+//    address; each lane adds the popcount of its row below bit 8 g. As in
+//    the paper, one rank serves every area stream; here the payload stores
+//    the two areas of an area row interleaved by rank, so that rank is one
+//    slot holding both values (area q = 2a, columns 8g..8g+7, and q = 2a + 1,
+//    columns 32+8g..32+8g+7), and one window of eight slots serves both
+//    areas. Active values are placed into their byte slots with four
+//    v_perm_b32 per window, selectors taken from a 256-entry table indexed by
+//    the 8-bit segment; inactive slots get selector 0x0C (zero). LTs are
+//    decoded in pairs so that two independent chains interleave.
 //
 //  * Row reordering (Section V-B). A reordered LT stores row pi[p] of the
 //    original LT as its row p, so union-mask row i pairs rows pi[i] and
@@ -100,19 +101,16 @@ constexpr int kMaxLds = 160 * 1024;
 
 // Selector pair for one 8-bit union-mask segment m. Slot s of the output
 // (dword 0: s = 0..3, dword 1: s = 4..7) holds segment position 2s (s < 4) or
-// 2(s-4)+1 (s >= 4). An active position of rank r takes the r-th packed
-// value: even r sits in byte r/2 of the "low" source, odd r in byte r/2 of the
-// "high" source (bytes 4..7 of v_perm_b32's 8-byte input).
+// 2(s-4)+1 (s >= 4). An active position of rank r takes the r-th value of its
+// area: byte r of the 8-byte plane v_perm_b32 reads (ranks 0..3 in the
+// "low" source, 4..7 in the "high" one).
 __device__ inline u32x2 perm_selectors(uint32_t m) {
     uint32_t sel[2] = {0u, 0u};
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
         const int pos = s < 4 ? 2 * s : 2 * (s - 4) + 1;
         uint32_t b = 0x0Cu;                                   // v_perm: constant zero
-        if ((m >> pos) & 1u) {
-            const uint32_t r = __popc(m & ((1u << pos) - 1u));
-            b = (r & 1u) ? 4u + (r >> 1) : (r >> 1);
-        }
+        if ((m >> pos) & 1u) b = __popc(m & ((1u << pos) - 1u));   // rank r: byte r of the slot planes
         sel[s >> 2] |= b << (8 * (s & 3));
     }
     return (u32x2){sel[0], sel[1]};
@@ -121,7 +119,7 @@ __device__ inline u32x2 perm_selectors(uint32_t m) {
 // LDS stage of one chunk of CH LTs (per wavefront), in bytes from the stage start:
 //   payload : the chunk's compressed values, streamed from the 16-byte
 //             boundary at or below the chunk's first byte (up to 15 bytes
-//             early); a segment window may read 8 bytes past the last value,
+//             early); a segment window may read 12 bytes past the last value,
 //             so a chunk needs at most 8 BITS CH + 2 pieces of 16 bytes (an
 //             LT holds at most 1024 values).
 //             Linear staging (RING = false) keeps the whole chunk. RING =
@@ -130,22 +128,20 @@ __device__ inline u32x2 perm_selectors(uint32_t m) {
 //             spans at most 128 BITS + 16 bytes with its window overhang, so
 //             the four slots hold every LT that is ready for decoding. The
 //             160 bytes after the ring repeat its first 160 bytes, so windows
-//             that start past the end of the ring (by at most one stream,
-//             32 BITS bytes, plus a window) read on into it;
+//             that start past the end of the ring (by at most one mask row's
+//             slots plus a window) read on into it;
 //   bitmaps : union-mask rows, 8 dwords per LT;
 //             (this and the next three arrays have room for a whole number
 //             of 4-LT passes; entries past the chunk are never decoded)
-//   bases   : per LT and lane row rr = 2i + a, the LDS bit address of the
-//             first value of row i in area stream 2a (folded into the ring
+//   bases   : per LT and lane row rr = 2i + a, the slot address of the
+//             first rank of mask row i in area row a (folded into the ring
 //             with RING; 16 dwords per LT);
-//   sd      : per LT, the number of bits of one area stream,
-//             BITS (o_{t+1} - o_t) / 4;
 //   offsets : o_t of the chunk's LTs and the end offset (CH + 1 dwords);
 //   (PERM: the bases area of LT j first holds its permutation word; after
 //   the row-base step the bitmap area holds per LT pair and lane row the two
-//   16-bit row bases, stage-relative bit addresses divided by 4, LT 2m in
-//   the low and LT 2m + 1 in the high half of the pair's dword, and the
-//   bases area the union-mask row that lane row decodes)
+//   16-bit row bases, stage-relative byte addresses, LT 2m in the low and
+//   LT 2m + 1 in the high half of the pair's dword, and the bases area the
+//   union-mask row that lane row decodes)
 //   X       : the chunk's activation slice, one row of 32 bytes per LT for
 //             each activation column; rows are 16 bytes longer than the
 //             slice so that the 16 rows read by one instruction fall in
@@ -160,10 +156,9 @@ struct Chunk {
     static constexpr int kLtPad = 4 * kPasses;                // per-LT arrays padded to whole passes
     static constexpr int kBmOffset = RING ? kRing + kGuard : 16 * kPayPieces;
     static constexpr int kBaseOffset = kBmOffset + 32 * kLtPad;
-    static constexpr int kSdOffset = kBaseOffset + 64 * kLtPad;
-    static constexpr int kOffOffset = kSdOffset + 4 * kLtPad;
+    static constexpr int kOffOffset = kBaseOffset + 64 * kLtPad;
     static constexpr int kXOffset = (kOffOffset + 4 * (kLtPad + 1) + 15) & ~15;
-    static_assert(!PERM || 8 * (RING ? kRing + kGuard : 16 * kPayPieces) <= 4 * 65536,
+    static_assert(!PERM || (RING ? kRing + kGuard : 16 * kPayPieces) <= 65536,
                   "16-bit row bases address the payload stage");
     static constexpr int kXRowWords = 8 * CH + 4;
     static constexpr int kXPieces = 2 * CH;                   // 16-byte pieces of one activation row
@@ -272,72 +267,91 @@ __device__ __forceinline__ uint32_t lane_value(uint32_t v, int lane) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
 
-// 32 bits of LDS starting at LDS bit address bn (payload value index * BITS,
-// relative to the stage).
-__device__ __forceinline__ uint32_t window(uint32_t bn) {
-    const uint2 d = lds_load2((bn >> 3) & ~3u);
-    return __builtin_amdgcn_alignbit(d.y, d.x, bn);
+// Rank slots. The payload stores the two areas of an area row interleaved by
+// rank (area (a, c) at value o_t + 4 a P_t + 2 rho + c), so rank rho of an
+// area row is one slot holding both of its values: a byte with 4-bit values
+// (area column 0 in the low nibble), a nibble with 2-bit values (area column
+// 0 in its low two bits). A slot address is an LDS byte address (4-bit) or
+// twice an LDS byte address plus the nibble (2-bit).
+template <int BITS>
+__device__ __forceinline__ uint32_t slot_dword(uint32_t s) {
+    return BITS == 4 ? (s & ~3u) : ((s >> 1) & ~3u);
 }
 
-// Eight packed INT4 values -> the two slot dwords of one segment
-// (even positions, odd positions).
-__device__ __forceinline__ int2 place(uint32_t w, uint2 sel) {
-    const uint32_t hi = w & kHiNib;            // odd ranks, already in the high nibble
-    const uint32_t lo = (w << 4) & kHiNib;     // even ranks moved up
-    return make_int2((int32_t)__builtin_amdgcn_perm(hi, lo, sel.x),
-                     (int32_t)__builtin_amdgcn_perm(hi, lo, sel.y));
+// The LDS dwords that hold the eight slots from slot address s: three dwords
+// for 4-bit slots (8 bytes at any byte offset), two for 2-bit ones.
+template <int BITS>
+struct SlotWin {
+    uint32_t d0, d1, d2;
+};
+template <int BITS>
+__device__ __forceinline__ SlotWin<BITS> slot_window(uint32_t s) {
+    const uint32_t a = slot_dword<BITS>(s);
+    const uint2 d = lds_load2(a);
+    SlotWin<BITS> w;
+    w.d0 = d.x;
+    w.d1 = d.y;
+    w.d2 = BITS == 4 ? lds_load(a + 8) : 0u;
+    return w;
 }
 
-// Eight packed 2-bit values (the low 16 bits of w) -> the two slot dwords
-// of one segment, each value in the top two bits of its byte (64 v). Byte j
-// of x takes nibble j of w (values 2j, 2j + 1 in its bits 0..3; its high
-// nibble is never used), then the odd and even values move to bits 6..7 of
-// byte j, which is where place() finds ranks 2j + 1 and 2j.
-__device__ __forceinline__ int2 place2(uint32_t w, uint2 sel) {
-    const uint32_t x = __builtin_amdgcn_perm(w >> 4, w, 0x05010400u);
-    const uint32_t hi = (x << 4) & 0xC0C0C0C0u;
-    const uint32_t lo = (x << 6) & 0xC0C0C0C0u;
-    return make_int2((int32_t)__builtin_amdgcn_perm(hi, lo, sel.x),
-                     (int32_t)__builtin_amdgcn_perm(hi, lo, sel.y));
+// Eight slots from slot address s -> the MFMA A operand of one segment: the
+// selector pair (positions -> ranks, 0x0C = zero) picks byte r of the
+// 8-byte plane of each area column, values moved to the high nibble (16 v)
+// or the top two bits (64 v) of their byte.
+template <int BITS>
+__device__ __forceinline__ i32x4 place_slots(SlotWin<BITS> d, uint32_t s, uint2 sel) {
+    uint32_t a0, a1, b0, b1;                               // area column 0 / 1 planes, ranks 0..3 / 4..7
+    if constexpr (BITS == 4) {
+        const uint32_t w0 = __builtin_amdgcn_alignbyte(d.d1, d.d0, s);
+        const uint32_t w1 = __builtin_amdgcn_alignbyte(d.d2, d.d1, s);
+        a0 = (w0 << 4) & kHiNib;
+        a1 = (w1 << 4) & kHiNib;
+        b0 = w0 & kHiNib;
+        b1 = w1 & kHiNib;
+    } else {
+        const uint32_t w = __builtin_amdgcn_alignbit(d.d1, d.d0, s << 2);
+        const uint32_t h = w >> 4;
+        const uint32_t x0 = __builtin_amdgcn_perm(h, w, 0x05010400u);   // byte j: slot j in bits 0..3
+        const uint32_t x1 = __builtin_amdgcn_perm(h, w, 0x07030602u);   // byte j: slot 4 + j
+        a0 = (x0 << 6) & 0xC0C0C0C0u;
+        a1 = (x1 << 6) & 0xC0C0C0C0u;
+        b0 = (x0 << 4) & 0xC0C0C0C0u;
+        b1 = (x1 << 4) & 0xC0C0C0C0u;
+    }
+    return (i32x4){(int32_t)__builtin_amdgcn_perm(a1, a0, sel.x), (int32_t)__builtin_amdgcn_perm(a1, a0, sel.y),
+                   (int32_t)__builtin_amdgcn_perm(b1, b0, sel.x), (int32_t)__builtin_amdgcn_perm(b1, b0, sel.y)};
+}
+
+// The selector pair of this lane's segment of mask row mrow; rot = (8 g - 3)
+// mod 32 puts segment g at bits 3..10, the table's byte offset.
+__device__ __forceinline__ uint2 selectors(const u32x2 *lut, uint32_t mrow, uint32_t rot) {
+    const u32x2 sv = *(const u32x2 *)((const char *)lut + (__builtin_amdgcn_alignbit(mrow, mrow, rot) & 0x7F8u));
+    return make_uint2(sv.x, sv.y);
 }
 
 // Decode one LT into the MFMA A operand of this lane.
 //   mrow : union-mask row i of the LT
-//   bn0  : LDS bit address of the first value of the lane's segment of row
-//          i in area stream 2a
-//   sd   : bits of one area stream (stream 2a + 1 starts sd bits later)
-//   rot  : (8 g - 3) mod 32, so that rotating mrow right by it puts the
-//          lane's segment at bits 3..10 (the selector table's byte offset)
+//   s    : slot address of the first rank of the lane's segment of row i
+//          in area row a
 template <int BITS>
-__device__ __forceinline__ i32x4 decode_at(const u32x2 *lut, uint32_t mrow, uint32_t bn0, uint32_t sd, uint32_t rot) {
-    const uint32_t bn1 = bn0 + sd;
-    const u32x2 sv = *(const u32x2 *)((const char *)lut + (__builtin_amdgcn_alignbit(mrow, mrow, rot) & 0x7F8u));
-    const uint2 sel = make_uint2(sv.x, sv.y);
-    int2 c0, c1;
-    if constexpr (BITS == 4) {
-        c0 = place(window(bn0), sel);
-        c1 = place(window(bn1), sel);
-    } else {
-        c0 = place2(window(bn0), sel);
-        c1 = place2(window(bn1), sel);
-    }
-    return (i32x4){c0.x, c0.y, c1.x, c1.y};
+__device__ __forceinline__ i32x4 decode_at(const u32x2 *lut, uint32_t mrow, uint32_t s, uint32_t rot) {
+    return place_slots<BITS>(slot_window<BITS>(s), s, selectors(lut, mrow, rot));
 }
 
-// The same from the row's base: the segment starts BITS x (active positions
-// of the row before it) bits further on.
+// The same from the row's base slot: the segment starts one slot per active
+// position of the row before it further on.
 template <int BITS>
-__device__ __forceinline__ i32x4 decode_tile(const u32x2 *lut, uint32_t mrow, uint32_t base, uint32_t sd,
-                                             uint32_t lomask, uint32_t rot) {
-    return decode_at<BITS>(lut, mrow, base + (uint32_t)BITS * __popc(mrow & lomask), sd, rot);
+__device__ __forceinline__ i32x4 decode_tile(const u32x2 *lut, uint32_t mrow, uint32_t base, uint32_t lomask,
+                                             uint32_t rot) {
+    return decode_at<BITS>(lut, mrow, base + (uint32_t)__popc(mrow & lomask), rot);
 }
 
-// The same for a 4-bit row base given as a stage-relative bit address / 4
-// (q) and the stage's bit address st8: the segment starts at
-// st8 + 4 (q + active positions before it).
-__device__ __forceinline__ i32x4 decode_tile_q(const u32x2 *lut, uint32_t mrow, uint32_t q, uint32_t st8, uint32_t sd,
+// The same for a 4-bit row base given as a stage-relative byte address q and
+// the stage's byte address st.
+__device__ __forceinline__ i32x4 decode_tile_q(const u32x2 *lut, uint32_t mrow, uint32_t q, uint32_t st,
                                                uint32_t lomask, uint32_t rot) {
-    return decode_at<4>(lut, mrow, st8 + ((q + (uint32_t)__popc(mrow & lomask)) << 2), sd, rot);
+    return decode_at<4>(lut, mrow, st + (q + (uint32_t)__popc(mrow & lomask)), rot);
 }
 
 // Dwords g and g + 4 of an activation row's 8 dwords for one LT.
@@ -395,7 +409,7 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
 
     const uint32_t st = lds0 + (uint32_t)(wave * stage_bytes);   // stage, LDS bytes
     const uint32_t st_bm = st + C::kBmOffset, st_base = st + C::kBaseOffset;
-    const uint32_t st_sd = st + C::kSdOffset, st_off = st + C::kOffOffset;
+    const uint32_t st_off = st + C::kOffOffset;
     const uint32_t st_x = st + C::kXOffset;
 
     // Activation reads in the decode: lane (column rr, k-group g) reads dwords
@@ -548,13 +562,18 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
         // area, the mask row into the LT's bases area. Every bitmap and
         // permutation word of the chunk is read before the first of them is
         // overwritten.
-        // Payload value v of the matrix is stream bit BITS v - 8 A0, at LDS
-        // bit address 8 st + (BITS v - 8 A0), taken mod 32768 with the ring.
-        const uint32_t rmask = RING ? 0x7FFFu : ~0u;
+        // Area row a's slots start P_t slots (2 P_t values) after area row
+        // 0's, and rank rho is slot rho of its area row: the scan injects P_t
+        // on area-row a = 1 lanes. Slot rho of LT t's area row 0 is slot
+        // o_t / 2 of the matrix; the chunk's stage starts at its byte A0
+        // (slot A0 * kSlotsPerByte), at stage slot address kSlotsPerByte st,
+        // taken mod the ring's slots with the ring.
+        constexpr uint32_t kSlotsPerByte = 4 / BITS;
+        const uint32_t smask = RING ? (uint32_t)C::kRing * kSlotsPerByte - 1u : ~0u;
         {
             const uint32_t jj = (uint32_t)lane >> 4;
             const uint32_t p_bm = st_bm + 32 * jj + 4 * i, p_off = st_off + 4 * jj;
-            const uint32_t q_base = st_base + 64 * jj, p_base = q_base + 4 * rr, p_sd = st_sd + 4 * jj;
+            const uint32_t q_base = st_base + 64 * jj, p_base = q_base + 4 * rr;
             const uint32_t q_b16 = st_bm + 64 * (jj >> 1) + 2 * (jj & 1), p_b16 = q_b16 + 4 * rr;
             const uint32_t p_pm = q_base + 4 * (rr & 1);
             uint32_t mrow[C::kPasses];
@@ -568,56 +587,53 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
             }
 #pragma unroll
             for (int ps = 0; ps < C::kPasses; ++ps) {
-                const uint32_t inj = amask & ((o[ps].y - o[ps].x) >> 1);
+                const uint32_t inj = amask & ((o[ps].y - o[ps].x) >> 2);    // P_t
                 uint32_t ex = (uint32_t)__builtin_amdgcn_update_dpp((int)inj, (int)__popc(mrow[ps]), 0x112, 0xF,
                                                                     0xF, false);
                 ex += dpp_row<0x112>(ex);
                 ex += dpp_row<0x114>(ex);
                 ex += dpp_row<0x118>(ex);
+                const uint32_t rel = ((o[ps].x >> 1) + ex - kSlotsPerByte * A0) & smask;   // stage slot
                 if constexpr (PERM) {
                     // The base is first written under this lane's own lane
                     // row, so that a word that is not a permutation still
                     // leaves every lane row with a base inside the stage.
-                    // (16 bits hold rel / 4: rel is a multiple of 4 below 8
-                    // x the payload area.)
+                    // (16 bits hold rel: a byte address below the payload
+                    // area's 64 KB.)
                     const uint32_t lr = (pm[ps] >> (4 * i)) & 15u;
-                    const uint16_t b16 = (uint16_t)((o[ps].x + ex - 2u * A0) & (rmask >> 2));   // rel / 4
+                    const uint16_t b16 = (uint16_t)rel;
                     lds_store16(p_b16 + 128 * ps, b16);
                     lds_store(q_base + 4 * lr + 256 * ps, mrow[ps]);
                     lds_store16(q_b16 + 4 * lr + 128 * ps, b16);
                 } else {
-                    const uint32_t rel = ((uint32_t)BITS * (o[ps].x + ex) - 8u * A0) & rmask;
-                    lds_store(p_base + 256 * ps, 8u * st + rel);
+                    lds_store(p_base + 256 * ps, kSlotsPerByte * st + rel);
                 }
-                if (rr == 0) lds_store(p_sd + 16 * ps, ((o[ps].y - o[ps].x) * (uint32_t)BITS) >> 2);
             }
         }
         // LT k can be decoded once the pieces holding its windows have landed:
-        // BITS o_{k+1} - 8 A0 + 64 <= 8192 (u + 1) stream bits, i.e. after
-        // load u = need_k.
-        const uint32_t need = ((uint32_t)BITS * lds_load(st_off + 4 * min(lane + 1, CH)) - 8u * A0 + 63u) >> 13;
+        // a window reads up to 12 (4-bit) or 8 (2-bit) bytes from a slot at
+        // most one past the LT's last, so BITS o_{k+1} - 8 A0 + 96 (64) <=
+        // 8192 (u + 1) stream bits, i.e. after load u = need_k.
+        constexpr uint32_t kOverhangBits = BITS == 4 ? 95u : 63u;
+        const uint32_t need =
+            ((uint32_t)BITS * lds_load(st_off + 4 * min(lane + 1, CH)) - 8u * A0 + kOverhangBits) >> 13;
 
-        // LDS addresses of the next LT's mask row, row base, stream length and
-        // activations for this lane; they advance as LTs are decoded. The
-        // stream-length address is the same on every lane; it is kept in a
-        // vector register so that the loop needs no scalar-to-vector moves.
-        // PERM reads the mask row routed to this lane row from the bases
-        // area and the 16-bit row bases of an LT pair from one dword of the
-        // bitmap area (pairs start at even LTs; a lone LT is the chunk's last,
-        // at an even position, in the low half).
-        uint32_t a_bm = st_bm + (PERM ? 4 * rr : 4 * i), a_base = st_base + 4 * rr, a_sd;
+        // LDS addresses of the next LT's mask row, row base and activations
+        // for this lane; they advance as LTs are decoded. PERM reads the mask
+        // row routed to this lane row from the bases area and the 16-bit row
+        // bases of an LT pair from one dword of the bitmap area (pairs start
+        // at even LTs; a lone LT is the chunk's last, at an even position, in
+        // the low half).
+        uint32_t a_bm = st_bm + (PERM ? 4 * rr : 4 * i), a_base = st_base + 4 * rr;
         auto row_at = [&](int k) { return PERM ? a_base + 64 * k : a_bm + 32 * k; };
-        const uint32_t st8 = 8u * st;
-        __asm__("v_mov_b32 %0, %1" : "=v"(a_sd) : "s"(st_sd));
         uint32_t a_x[NB];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) a_x[nb] = xq[nb];
         auto decode_one = [&]() {
             const uint32_t mrow = lds_load(row_at(0));
-            const uint32_t sd = lds_load(a_sd);
             i32x4 A;
-            if constexpr (PERM) A = decode_tile_q(lut, mrow, lds_load(a_bm) & 0xFFFFu, st8, sd, lomask, rot);
-            else A = decode_tile<BITS>(lut, mrow, lds_load(a_base), sd, lomask, rot);
+            if constexpr (PERM) A = decode_tile_q(lut, mrow, lds_load(a_bm) & 0xFFFFu, st, lomask, rot);
+            else A = decode_tile<BITS>(lut, mrow, lds_load(a_base), lomask, rot);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
                 acc[nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, unpack_x(x_pair(a_x[nb])), acc[nb], 0, 0, 0);
@@ -625,19 +641,17 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
             }
             a_bm += 32;
             a_base += 64;
-            a_sd += 4;
         };
         auto decode_two = [&]() {
             const uint32_t m0 = lds_load(row_at(0)), m1 = lds_load(row_at(1));
-            const uint2 sd = lds_load2(a_sd);
             i32x4 A0v, A1v;
             if constexpr (PERM) {
                 const uint32_t w = lds_load(a_bm);
-                A0v = decode_tile_q(lut, m0, w & 0xFFFFu, st8, sd.x, lomask, rot);
-                A1v = decode_tile_q(lut, m1, w >> 16, st8, sd.y, lomask, rot);
+                A0v = decode_tile_q(lut, m0, w & 0xFFFFu, st, lomask, rot);
+                A1v = decode_tile_q(lut, m1, w >> 16, st, lomask, rot);
             } else {
-                A0v = decode_tile<BITS>(lut, m0, lds_load(a_base), sd.x, lomask, rot);
-                A1v = decode_tile<BITS>(lut, m1, lds_load(a_base + 64), sd.y, lomask, rot);
+                A0v = decode_tile<BITS>(lut, m0, lds_load(a_base), lomask, rot);
+                A1v = decode_tile<BITS>(lut, m1, lds_load(a_base + 64), lomask, rot);
             }
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
@@ -647,7 +661,6 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
             }
             a_bm += 64;
             a_base += 128;
-            a_sd += 8;
         };
 
         // The payload lands in issue order: after load u, stream bytes

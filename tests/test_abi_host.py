@@ -15,6 +15,10 @@ import pytest
 from oracle import iebme
 from paper_2608_09291_amd import binding, synth
 
+# The value order the library's encoders write: the areas of an area row
+# interleaved by rank.
+LIB_ORDER = "area_rows"
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
@@ -54,7 +58,7 @@ def _assert_same_encoding(enc, ref):
     (256, 512, 0.6, 6, True), (512, 512, 0.5, 7, False)])
 def test_encoder_matches_oracle(M, K, s, seed, skew):
     W, _, _ = synth.random_problem(M, K, 1, s, seed, row_skew=skew)
-    _assert_same_encoding(binding.encode(W), iebme.encode(W))
+    _assert_same_encoding(binding.encode(W), iebme.encode(W, order=LIB_ORDER))
 
 
 def test_encoder_matches_oracle_worked_tile(golden):
@@ -68,14 +72,14 @@ def test_encoder_matches_oracle_worked_tile(golden):
                 q = int(rng.integers(4))
                 a, c = divmod(q, 2)
                 W[8 * a + i, 32 * c + j] = synth.nonzero_int4(rng, 1)[0]
-    _assert_same_encoding(binding.encode(W), iebme.encode(W))
+    _assert_same_encoding(binding.encode(W), iebme.encode(W, order=LIB_ORDER))
 
 
 @pytest.mark.slow
 def test_encoder_matches_oracle_full_size():
     w = synth.WORKLOADS["ffn_down_4096x11008_s50"]
     W = synth.weights(w)
-    enc, ref = binding.encode(W), iebme.encode(W)
+    enc, ref = binding.encode(W), iebme.encode(W, order=LIB_ORDER)
     _assert_same_encoding(enc, ref)
     rep = binding.pmr(enc, N=8)
     assert rep["pmr"] == pytest.approx(iebme.pmr_report(ref, N=8)["pmr"], rel=1e-12)
@@ -84,7 +88,7 @@ def test_encoder_matches_oracle_full_size():
 @pytest.mark.parametrize("N", [0, 1, 8, 32])
 def test_pmr_matches_oracle(N):
     W, _, _ = synth.random_problem(128, 512, 1, 0.5, 9)
-    enc, ref = binding.encode(W), iebme.encode(W)
+    enc, ref = binding.encode(W), iebme.encode(W, order=LIB_ORDER)
     got, want = binding.pmr(enc, N), iebme.pmr_report(ref, N)
     for key in ("nnz", "stored_values", "n_lt", "payload_stored_bytes", "bitmap_bytes",
                 "offset_bytes", "meta_bytes"):
@@ -151,7 +155,7 @@ def test_encode_with_row_stride():
     s = binding.IEBME()
     assert binding.lib().us_encode(big.ctypes.data, 32, 128, 200, ctypes.byref(s)) == 0
     enc = binding.Encoded(s)
-    _assert_same_encoding(enc, iebme.encode(W))
+    _assert_same_encoding(enc, iebme.encode(W, order=LIB_ORDER))
 
 
 def _dev_struct(M=32, K=128, n_lt=None, n_payload=0, ptr=0x1000):

@@ -17,7 +17,7 @@ from paper_2608_09291_amd import binding, synth
 
 def _check_against_oracle(W):
     enc = binding.encode(W, reorder=True)
-    ref, perms = reorder.encode_reordered(W)
+    ref, perms = reorder.encode_reordered(W, order="area_rows")
     assert enc.n_lt == ref.n_lt and enc.nnz == ref.nnz and enc.n_payload == ref.n_payload
     assert np.array_equal(enc.perm, reorder.perm_words(perms))
     assert np.array_equal(enc.bitmaps, ref.bitmaps)

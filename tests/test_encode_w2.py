@@ -19,7 +19,7 @@ from paper_2608_09291_amd import binding, synth
     (256, 512, 0.6, 6, True), (512, 512, 0.5, 7, False)])
 def test_w2_encoder_matches_oracle(M, K, s, seed, skew):
     W, _, _ = synth.random_problem(M, K, 1, s, seed, row_skew=skew, bits=2)
-    enc, ref = binding.encode(W, bits=2), iebme.encode(W, bits=2)
+    enc, ref = binding.encode(W, bits=2), iebme.encode(W, bits=2, order="area_rows")
     assert enc.bits == 2 and enc.perm is None
     assert enc.n_lt == ref.n_lt and enc.nnz == ref.nnz and enc.n_payload == ref.n_payload
     assert np.array_equal(enc.bitmaps, ref.bitmaps)
@@ -30,7 +30,7 @@ def test_w2_encoder_matches_oracle(M, K, s, seed, skew):
 @pytest.mark.parametrize("N", [0, 1, 8, 32])
 def test_w2_pmr_matches_oracle(N):
     W, _, _ = synth.random_problem(128, 512, 1, 0.5, 9, bits=2)
-    got, want = binding.pmr(binding.encode(W, bits=2), N), iebme.pmr_report(iebme.encode(W, bits=2), N)
+    got, want = binding.pmr(binding.encode(W, bits=2), N), iebme.pmr_report(iebme.encode(W, bits=2, order="area_rows"), N)
     for key in ("nnz", "stored_values", "n_lt", "payload_stored_bytes", "bitmap_bytes", "offset_bytes",
                 "meta_bytes"):
         assert got[key] == want[key], key
@@ -56,7 +56,7 @@ def test_w2_refuses_reordering_in_the_binding():
 def test_w2_encoder_full_size():
     w = synth.WORKLOADS["ffn_down_4096x11008_s50"]
     W = synth.weights(w, bits=2)
-    enc, ref = binding.encode(W, bits=2), iebme.encode(W, bits=2)
+    enc, ref = binding.encode(W, bits=2), iebme.encode(W, bits=2, order="area_rows")
     assert np.array_equal(enc.offsets, ref.offsets)
     assert np.array_equal(enc.payload, ref.payload)
     assert np.array_equal(enc.bitmaps, ref.bitmaps)
