@@ -1,7 +1,8 @@
-// IE-BME x INT4 -> INT32 sparse product on gfx950 (CDNA4): the kernel and
-// its launch templates, shared by us_spmm.hip (4-bit weights, rows in stored
-// order), us_spmm_perm.hip (row-reordered LTs) and us_spmm_w2.hip (2-bit
-// weights).
+// IE-BME x INT4 -> INT32 sparse product on gfx950 (CDNA4): the chunked
+// kernel and its launch templates, instantiated by us_spmm.hip (4-bit
+// weights, rows in stored order), us_spmm_narrow.hip (the same for N <= 4),
+// us_spmm_perm.hip (row-reordered LTs) and us_spmm_w2.hip (2-bit weights);
+// the single-pass family (us_spmm_burst.h) shares its decode helpers.
 //
 // The operation is the UnionSparse kernel of Section VI: Y = W X with W in
 // IE-BME (Section V-A), X dense INT4, INT32 accumulation. What is kept from
