@@ -2,7 +2,7 @@
 
 Each kernel instantiation is built for a number of resident wavefronts per
 SIMD (its launch bound), and the host's configuration choice counts on that
-residency. This test compiles the four kernel translation units to
+residency. This test compiles every kernel translation unit to
 assembly and checks, for every instantiation, that its VGPRs fit that many
 wavefronts (512 per SIMD lane, in granules of 8; the kernels use no AGPRs,
 so the VGPR count is the whole register budget) and that it needs no
@@ -26,9 +26,6 @@ UNITS = ("us_dense", "us_spmm", "us_spmm_narrow", "us_spmm_perm", "us_spmm_w2", 
 FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fno-strict-aliasing", "-Xclang", "-target-feature",
          "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"), "-I", CSRC, "--cuda-device-only", "-S"]
 
-# The reordered kernels above 16 columns with 8-LT multi-chunk slices keep
-# 8 bytes in scratch at their 128-VGPR budget.
-KNOWN_SPILLS = {(32, 8, True, False, True)}
 
 
 def waves_per_simd(wpg, nmax, ch, multi, ring, perm):
@@ -135,7 +132,6 @@ def test_registers_fit_the_residency_the_host_assumes(kernel_list):
     assert not over, over[:5]
 
 
-def test_no_scratch_except_the_known_case(kernel_list):
-    spills = [k for k in kernel_list if k["scratch"]
-              and (k["nmax"], k["ch"], k["multi"], k["ring"], k["perm"]) not in KNOWN_SPILLS]
+def test_no_kernel_needs_scratch(kernel_list):
+    spills = [k for k in kernel_list if k["scratch"]]
     assert not spills, spills[:5]
