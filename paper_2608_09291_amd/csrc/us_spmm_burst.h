@@ -194,7 +194,7 @@ __global__ __launch_bounds__(64 * WPG, burst_waves_per_simd(WPG, NMAX)) void us_
         float, __builtin_amdgcn_raw_buffer_load_b32(ssrc, (uint32_t)(4 * (mb * 16 + (int)(threadIdx.x & 15))), 0, 0));
 
     // Selector table, computed while the requests fly.
-    for (int e = threadIdx.x; e < 256; e += 64 * WPG) lut[e] = perm_selectors((uint32_t)e);
+    for (int e = threadIdx.x; e < 256; e += 64 * WPG) lut[e] = perm_selectors<BITS>((uint32_t)e);
     // The youngest wavefronts of a CU, which its SIMDs' arbiters serve last,
     // start at a higher issue priority: the workgroup's dispatch round
     // (blockIdx / CUs) plus the wavefront's place among the workgroup's
@@ -311,11 +311,11 @@ __global__ __launch_bounds__(64 * WPG, burst_waves_per_simd(WPG, NMAX)) void us_
         row_of(std::integral_constant<int, j + 1>(), m1, b1);
         const uint32_t p0 = b0 + (uint32_t)__popc(m0 & lomask);
         const uint32_t p1 = b1 + (uint32_t)__popc(m1 & lomask);
-        const SlotWin<BITS> w0 = slot_window<BITS>(p0), w1 = slot_window<BITS>(p1);
+        const uint2 w0 = slot_window<BITS>(p0), w1 = slot_window<BITS>(p1);
         const uint2 e0 = selectors(lut, m0, rot), e1 = selectors(lut, m1, rot);
         const uint2 x0 = x_of(std::integral_constant<int, j>()), x1 = x_of(std::integral_constant<int, j + 1>());
-        const i32x4 A0v = place_slots<BITS>(w0, p0, e0);
-        const i32x4 A1v = place_slots<BITS>(w1, p1, e1);
+        const i32x4 A0v = place_slots<BITS>(w0, e0);
+        const i32x4 A1v = place_slots<BITS>(w1, e1);
         acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0v, unpack_x2(x0), acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1v, unpack_x2(x1), acc, 0, 0, 0);
     };

@@ -100,18 +100,25 @@ constexpr int kBufferDword3 = 0x00020000;              // raw buffer, 32-bit dat
 constexpr int kLutBytes = 2048;                        // 256 selector pairs (static LDS)
 constexpr int kMaxLds = 160 * 1024;
 
-// Selector pair for one 8-bit union-mask segment m. Slot s of the output
+// Selector pair for one 8-bit union-mask segment m. Byte s of the output
 // (dword 0: s = 0..3, dword 1: s = 4..7) holds segment position 2s (s < 4) or
-// 2(s-4)+1 (s >= 4). An active position of rank r takes the r-th value of its
-// area: byte r of the 8-byte plane v_perm_b32 reads (ranks 0..3 in the
-// "low" source, 4..7 in the "high" one).
+// 2(s-4)+1 (s >= 4). An active position of rank r takes the r-th slot of
+// the window, which v_perm_b32 reads from the 8 bytes it is given: with
+// 4-bit values byte r of the window (slots 0..3 in the "low" source, 4..7
+// in the "high" one); with 2-bit values the window w and w >> 4 hold slot r
+// in the low nibble of byte r / 2 of w (r even) or of w >> 4 (r odd, the
+// "high" source).
+template <int BITS>
 __device__ inline u32x2 perm_selectors(uint32_t m) {
     uint32_t sel[2] = {0u, 0u};
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
         const int pos = s < 4 ? 2 * s : 2 * (s - 4) + 1;
         uint32_t b = 0x0Cu;                                   // v_perm: constant zero
-        if ((m >> pos) & 1u) b = __popc(m & ((1u << pos) - 1u));   // rank r: byte r of the slot planes
+        if ((m >> pos) & 1u) {
+            const uint32_t r = __popc(m & ((1u << pos) - 1u));
+            b = BITS == 4 ? r : (r & 1u) * 4u + (r >> 1);
+        }
         sel[s >> 2] |= b << (8 * (s & 3));
     }
     return (u32x2){sel[0], sel[1]};
@@ -274,54 +281,43 @@ __device__ __forceinline__ uint32_t lane_value(uint32_t v, int lane) {
 // (area column 0 in the low nibble), a nibble with 2-bit values (area column
 // 0 in its low two bits). A slot address is an LDS byte address (4-bit) or
 // twice an LDS byte address plus the nibble (2-bit).
+//
+// The eight slots from slot address s, as two dwords (slots 0..3, 4..7):
+// 4-bit slots are the 8 bytes at s, aligned from the three dwords that hold
+// them (an unaligned 8-byte LDS read gives the same bytes but takes far
+// longer); 2-bit slots are the 32 bits at nibble s, taken from the two
+// dwords that hold them, and returned with the same bits shifted down by
+// one nibble (see perm_selectors).
 template <int BITS>
-__device__ __forceinline__ uint32_t slot_dword(uint32_t s) {
-    return BITS == 4 ? (s & ~3u) : ((s >> 1) & ~3u);
-}
-
-// The LDS dwords that hold the eight slots from slot address s: three dwords
-// for 4-bit slots (8 bytes at any byte offset), two for 2-bit ones.
-template <int BITS>
-struct SlotWin {
-    uint32_t d0, d1, d2;
-};
-template <int BITS>
-__device__ __forceinline__ SlotWin<BITS> slot_window(uint32_t s) {
-    const uint32_t a = slot_dword<BITS>(s);
-    const uint2 d = lds_load2(a);
-    SlotWin<BITS> w;
-    w.d0 = d.x;
-    w.d1 = d.y;
-    w.d2 = BITS == 4 ? lds_load(a + 8) : 0u;
-    return w;
-}
-
-// Eight slots from slot address s -> the MFMA A operand of one segment: the
-// selector pair (positions -> ranks, 0x0C = zero) picks byte r of the
-// 8-byte plane of each area column, values moved to the high nibble (16 v)
-// or the top two bits (64 v) of their byte.
-template <int BITS>
-__device__ __forceinline__ i32x4 place_slots(SlotWin<BITS> d, uint32_t s, uint2 sel) {
-    uint32_t a0, a1, b0, b1;                               // area column 0 / 1 planes, ranks 0..3 / 4..7
+__device__ __forceinline__ uint2 slot_window(uint32_t s) {
     if constexpr (BITS == 4) {
-        const uint32_t w0 = __builtin_amdgcn_alignbyte(d.d1, d.d0, s);
-        const uint32_t w1 = __builtin_amdgcn_alignbyte(d.d2, d.d1, s);
-        a0 = (w0 << 4) & kHiNib;
-        a1 = (w1 << 4) & kHiNib;
-        b0 = w0 & kHiNib;
-        b1 = w1 & kHiNib;
+        const uint32_t a = s & ~3u;
+        const uint2 d = lds_load2(a);
+        const uint32_t d2 = lds_load(a + 8);
+        return make_uint2(__builtin_amdgcn_alignbyte(d.y, d.x, s), __builtin_amdgcn_alignbyte(d2, d.y, s));
     } else {
-        const uint32_t w = __builtin_amdgcn_alignbit(d.d1, d.d0, s << 2);
-        const uint32_t h = w >> 4;
-        const uint32_t x0 = __builtin_amdgcn_perm(h, w, 0x05010400u);   // byte j: slot j in bits 0..3
-        const uint32_t x1 = __builtin_amdgcn_perm(h, w, 0x07030602u);   // byte j: slot 4 + j
-        a0 = (x0 << 6) & 0xC0C0C0C0u;
-        a1 = (x1 << 6) & 0xC0C0C0C0u;
-        b0 = (x0 << 4) & 0xC0C0C0C0u;
-        b1 = (x1 << 4) & 0xC0C0C0C0u;
+        const uint2 d = lds_load2((s >> 1) & ~3u);
+        const uint32_t w = __builtin_amdgcn_alignbit(d.y, d.x, s << 2);
+        return make_uint2(w, w >> 4);
     }
-    return (i32x4){(int32_t)__builtin_amdgcn_perm(a1, a0, sel.x), (int32_t)__builtin_amdgcn_perm(a1, a0, sel.y),
-                   (int32_t)__builtin_amdgcn_perm(b1, b0, sel.x), (int32_t)__builtin_amdgcn_perm(b1, b0, sel.y)};
+}
+
+// Eight slots -> the MFMA A operand of one segment: the selector pair picks
+// the byte holding each position's slot (0x0C = zero), and each area
+// column's value is moved to the high nibble (16 v) or the top two bits
+// (64 v) of its byte.
+template <int BITS>
+__device__ __forceinline__ i32x4 place_slots(uint2 w, uint2 sel) {
+    const uint32_t p0 = __builtin_amdgcn_perm(w.y, w.x, sel.x);
+    const uint32_t p1 = __builtin_amdgcn_perm(w.y, w.x, sel.y);
+    if constexpr (BITS == 4) {
+        return (i32x4){(int32_t)((p0 << 4) & kHiNib), (int32_t)((p1 << 4) & kHiNib), (int32_t)(p0 & kHiNib),
+                       (int32_t)(p1 & kHiNib)};
+    } else {
+        constexpr uint32_t kTop2 = 0xC0C0C0C0u;
+        return (i32x4){(int32_t)((p0 << 6) & kTop2), (int32_t)((p1 << 6) & kTop2), (int32_t)((p0 << 4) & kTop2),
+                       (int32_t)((p1 << 4) & kTop2)};
+    }
 }
 
 // The selector pair of this lane's segment of mask row mrow; rot = (8 g - 3)
@@ -337,7 +333,7 @@ __device__ __forceinline__ uint2 selectors(const u32x2 *lut, uint32_t mrow, uint
 //          in area row a
 template <int BITS>
 __device__ __forceinline__ i32x4 decode_at(const u32x2 *lut, uint32_t mrow, uint32_t s, uint32_t rot) {
-    return place_slots<BITS>(slot_window<BITS>(s), s, selectors(lut, mrow, rot));
+    return place_slots<BITS>(slot_window<BITS>(s), selectors(lut, mrow, rot));
 }
 
 // The same from the row's base slot: the segment starts one slot per active
@@ -380,7 +376,7 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     constexpr int NB = NMAX > 16 ? 2 : 1;                 // MFMA column blocks
     using C = Chunk<CH, RING, PERM, BITS>;
     static_assert(BITS == 4 || BITS == 2, "payload values are 4 or 2 bits");
-    static_assert(!PERM || BITS == 4, "16-bit row bases hold stage bit addresses / 4 (4-bit values)");
+    static_assert(!PERM || BITS == 4, "16-bit row bases hold stage-relative byte slots (4-bit values)");
     constexpr int kValShift = BITS == 4 ? 1 : 2;          // log2(values per byte)
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
     __shared__ u32x2 lut[256];                               // selector table
@@ -467,7 +463,7 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     float row_scale = 0.0f;
     if (p.scale && (int)threadIdx.x < 16 * N) row_scale = p.scale[(int64_t)mb * 16 + (threadIdx.x & 15)];
     // Selector table, computed while the first requests fly.
-    for (int e = threadIdx.x; e < 256; e += 64 * WPG) lut[e] = perm_selectors((uint32_t)e);
+    for (int e = threadIdx.x; e < 256; e += 64 * WPG) lut[e] = perm_selectors<BITS>((uint32_t)e);
     __syncthreads();
     __builtin_amdgcn_sched_barrier(0);                     // nothing that waits on the inputs moves above
 
@@ -554,15 +550,14 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     auto decode_chunk = [&]() {
 
         // Row bases: lanes 16 jj + rr handle LT j = 4 pass + jj, mask row i,
-        // area row a. The scan over the 16 lanes of a DPP row starts area row
-        // a = 1 at 2 P_t (its streams follow streams 0 and 1) and adds the
+        // area row a. The scan over the 16 lanes of a DPP row adds the
         // popcounts of the rows before i. With PERM the row base and the
         // mask row of (i, a), i.e. of reordered row 8a + i, go to the lane
         // row of original row r = pi[8a + i]: 2 (r mod 8) + r / 8; the row
-        // base (as a 16-bit stage bit address / 4) into the LT pair's bitmap
-        // area, the mask row into the LT's bases area. Every bitmap and
-        // permutation word of the chunk is read before the first of them is
-        // overwritten.
+        // base (as a 16-bit slot address relative to the stage) into the LT
+        // pair's bitmap area, the mask row into the LT's bases area. Every
+        // bitmap and permutation word of the chunk is read before the first
+        // of them is overwritten.
         // Area row a's slots start P_t slots (2 P_t values) after area row
         // 0's, and rank rho is slot rho of its area row: the scan injects P_t
         // on area-row a = 1 lanes. Slot rho of LT t's area row 0 is slot
