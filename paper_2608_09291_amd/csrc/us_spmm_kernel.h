@@ -23,12 +23,14 @@
 //    were requested together with the offsets, are copied into the
 //    wavefront's own LDS stage. The payload is staged whole (loaded straight
 //    into LDS up to 16 activation columns, via registers above) or through
-//    a 4 KB ring via registers (see Chunk); a slice of
-//    several chunks requests the next chunk's inputs ahead of the current
-//    payload. Only the wavefront itself reads its stage: its vmcnt waits and
-//    its in-order LDS accesses order staging before decoding, with no
-//    workgroup barrier. The host picks the split, the chunk length and the
-//    staging per shape (choose_config).
+//    a 4 KB ring via registers (see Chunk). A slice of several chunks
+//    requests the next chunk's inputs ahead of the current payload; above
+//    16 activation columns it also requests the next chunk's first payload
+//    pieces during the current chunk's last steps, so that its payload
+//    streams on across chunk boundaries (kPipe). Only the wavefront itself
+//    reads its stage: its vmcnt waits and its in-order LDS accesses order
+//    staging before decoding, with no workgroup barrier. The host picks the
+//    split, the chunk length and the staging per shape (choose_config).
 //
 //  * Decode (the paper's LSPD, Section VI-B). One LT (16 x 64) is decoded by
 //    one wavefront straight into the A operand of v_mfma_i32_16x16x64_i8.
@@ -375,6 +377,16 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     SpmmArgs p, int stage_bytes) {
     constexpr int NB = NMAX > 16 ? 2 : 1;                 // MFMA column blocks
     using C = Chunk<CH, RING, PERM, BITS>;
+    // Pipelined chunks: slices of several chunks whose payload passes through
+    // registers into linear staging (the kernels above 16 activation columns)
+    // request the first pieces of their next chunk while the current chunk's
+    // last pieces are decoded, so that a slice's payload streams without a
+    // round trip at every chunk boundary. Their loads are all visible to the
+    // compiler, whose own waits then order every use exactly. (Not for
+    // reordered 8-LT chunks: the next chunk's pieces would not fit their
+    // register budget.)
+    constexpr bool kPipe = MULTI && !RING && NMAX > 16 && !(PERM && CH > 4);
+    static_assert(!kPipe || C::kLoads >= kWindow, "a pipelined chunk takes at least one window of pieces");
     static_assert(BITS == 4 || BITS == 2, "payload values are 4 or 2 bits");
     static_assert(!PERM || BITS == 4, "16-bit row bases hold stage-relative byte slots (4-bit values)");
     constexpr int kValShift = BITS == 4 ? 1 : 2;          // log2(values per byte)
@@ -422,8 +434,10 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
         __builtin_amdgcn_make_buffer_rsrc((void *)p.x, (short)0, N * xrow_bytes, kBufferDword3);
     // Activation staging: the chunk's N x 2 CH pieces of 16 bytes, piece
     // q = lane + 64 u is row q / (2 CH), piece q % (2 CH). Only the loads
-    // that carry pieces are issued: the texture path, not HBM, limits how
-    // fast a CU takes them in at the start of the kernel.
+    // that carry pieces are issued (all of them in pipelined slices, whose
+    // wait counts must not depend on N: the others read zero, with no
+    // memory traffic): the texture path, not HBM, limits how fast a CU takes
+    // them in at the start of the kernel.
     constexpr int kXLoads = (NMAX * C::kXPieces + 63) / 64;
     const int x_loads = (N * C::kXPieces + 63) / 64;                           // wave-uniform
     uint32_t xv[kXLoads], xs[kXLoads];                     // global byte offset, LDS address
@@ -453,7 +467,7 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
         const uint32_t xk = (uint32_t)(32 * (kb0 + c0));
 #pragma unroll
         for (int u = 0; u < kXLoads; ++u)
-            if (u < x_loads) px[u] = __builtin_amdgcn_raw_buffer_load_b128(xsrc, xv[u] + xk, 0, 0);
+            if (kPipe || u < x_loads) px[u] = __builtin_amdgcn_raw_buffer_load_b128(xsrc, xv[u] + xk, 0, 0);
     };
 
     request(0);
@@ -482,6 +496,8 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     auto load_piece = [&](int u) {
         pf[u] = __builtin_amdgcn_raw_buffer_load_b128(psrc, (uint32_t)(16 * lane + 1024 * u), 0, kNonTemporal);
     };
+    [[maybe_unused]] uint32_t A0n = 0;                     // (kPipe) the next chunk's first staged byte
+    [[maybe_unused]] __amdgpu_buffer_rsrc_t psrcn;         // (kPipe) and its payload range
     constexpr bool kDirect = !RING && NMAX <= 16;         // payload straight into LDS
     auto dma_piece = [&](auto uc) {
         constexpr int u = decltype(uc)::value;
@@ -489,6 +505,42 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
             dma16(pdesc, st + 1024u * u, (uint32_t)(16 * lane), 1024u * u);
     };
 
+    // Bitmaps (zero past the chunk), offsets and activations into the stage.
+    auto commit_inputs = [&]() {
+        if (lane < 2 * CH) lds_store4(st_bm + 16 * lane, lane < 2 * cnt ? pbm : (u32x4){0u, 0u, 0u, 0u});
+        if (lane <= CH) lds_store(st_off + 4 * lane, offv);
+        if constexpr (PERM) {
+            // The lane row of original row r is 2 (r mod 8) + r / 8,
+            // r's 4 bits rotated left by one: done here for every
+            // nibble at once.
+            auto lane_rows = [](uint32_t w) { return ((w << 1) & 0xEEEEEEEEu) | ((w >> 3) & 0x11111111u); };
+            if (lane < CH) lds_store2(st_base + 64 * lane, (u32x2){lane_rows(pperm.x), lane_rows(pperm.y)});
+        }
+#pragma unroll
+        for (int u = 0; u < kXLoads; ++u)
+            if (u < x_loads && xs[u] != 0u) lds_store4(xs[u], (u32x4)px[u]);
+    };
+    // (kPipe) Stage a chunk of a pipelined slice; NX: another chunk follows.
+    // The first chunk requests its first pieces here; a later chunk's were
+    // requested during the previous chunk's decode. Either way the next
+    // chunk's inputs are requested after this chunk's first pieces.
+    auto stage_pipe = [&](int c0, auto nx, auto first) {
+        cnt = min(CH, nlt - c0);
+        if constexpr (decltype(first)::value) {
+            wait_vm_all();                                 // offsets, bitmaps, activations
+            const uint32_t ob = lane_value(offv, 0), oe = lane_value(offv, cnt);
+            A0 = us_range::first_byte<BITS>(ob, (uint32_t)p.pay_bytes);
+            const uint32_t prange =
+                us_range::range_bytes<BITS>(oe, A0, (uint32_t)p.pay_bytes, (uint32_t)C::kPayPieces);
+            psrc = __builtin_amdgcn_make_buffer_rsrc((void *)(p.pay + A0), (short)0, (int)prange, kBufferDword3);
+            static_for<0, kWindow>([&](auto uc) { load_piece(decltype(uc)::value); });
+        } else {
+            A0 = A0n;
+            psrc = psrcn;
+        }
+        commit_inputs();
+        if constexpr (decltype(nx)::value) request(c0 + CH);
+    };
     auto stage_chunk = [&](int c0) {
         cnt = min(CH, nlt - c0);
         wait_vm_all();                                     // offsets, bitmaps, activations
@@ -519,21 +571,6 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
                 }
             });
         };
-        // Bitmaps (zero past the chunk), offsets and activations into the stage.
-        auto commit_inputs = [&]() {
-            if (lane < 2 * CH) lds_store4(st_bm + 16 * lane, lane < 2 * cnt ? pbm : (u32x4){0u, 0u, 0u, 0u});
-            if (lane <= CH) lds_store(st_off + 4 * lane, offv);
-            if constexpr (PERM) {
-                // The lane row of original row r is 2 (r mod 8) + r / 8,
-                // r's 4 bits rotated left by one: done here for every
-                // nibble at once.
-                auto lane_rows = [](uint32_t w) { return ((w << 1) & 0xEEEEEEEEu) | ((w >> 3) & 0x11111111u); };
-                if (lane < CH) lds_store2(st_base + 64 * lane, (u32x2){lane_rows(pperm.x), lane_rows(pperm.y)});
-            }
-#pragma unroll
-            for (int u = 0; u < kXLoads; ++u)
-                if (u < x_loads && xs[u] != 0u) lds_store4(xs[u], (u32x4)px[u]);
-        };
         if (MULTI && nlt - c0 > CH) {
             // A later chunk follows: once this chunk's inputs are in LDS their
             // registers take the next chunk's inputs, requested ahead of this
@@ -547,7 +584,9 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
         }
     };
 
-    auto decode_chunk = [&]() {
+    // NX: (kPipe) another chunk of the slice follows this one.
+    auto decode_chunk = [&](int c0, auto nx) {
+        constexpr bool NX = decltype(nx)::value;
 
         // Row bases: lanes 16 jj + rr handle LT j = 4 pass + jj, mask row i,
         // area row a. The scan over the 16 lanes of a DPP row adds the
@@ -666,14 +705,40 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
         // step at most (the partner spans at most 528 more bytes). With the
         // ring the chunk's last LT goes alone as soon as it is ready, as
         // later steps may refill its slots.
+        //
+        // (kPipe, NX) Once all of this chunk's pieces are requested, each
+        // step requests one of the next chunk's first kWindow pieces instead,
+        // into the registers of pieces already staged; the next chunk's
+        // payload range comes from its offsets, requested with this chunk's
+        // inputs.
         int j = 0;
+        if constexpr (kPipe && NX) {
+            const int cn = min(CH, nlt - c0 - CH);
+            const uint32_t obn = lane_value(offv, 0), oen = lane_value(offv, cn);
+            A0n = us_range::first_byte<BITS>(obn, (uint32_t)p.pay_bytes);
+            const uint32_t prn = us_range::range_bytes<BITS>(oen, A0n, (uint32_t)p.pay_bytes, (uint32_t)C::kPayPieces);
+            psrcn = __builtin_amdgcn_make_buffer_rsrc((void *)(p.pay + A0n), (short)0, (int)prn, kBufferDword3);
+        }
         static_for<0, C::kLoads>([&](auto uc) {
             constexpr int u = decltype(uc)::value;
-            constexpr int later = (kWindow - 1 < C::kLoads - 1 - u) ? kWindow - 1 : C::kLoads - 1 - u;
-            wait_vm<later>();                              // piece u has landed
-            if constexpr (kDirect) {
+            [[maybe_unused]] constexpr int later = (kWindow - 1 < C::kLoads - 1 - u) ? kWindow - 1 : C::kLoads - 1 - u;
+            if constexpr (kPipe) {
+                // Piece u into the stage, then the next request (which may
+                // reuse piece u's registers).
+                if (u + 1 < C::kLoads || lane + 64 * u < C::kPayPieces)
+                    lds_store4(st + 1024 * u + 16 * lane, (u32x4)pf[u]);
+                if constexpr (u + kWindow < C::kLoads) {
+                    load_piece(u + kWindow);
+                } else if constexpr (NX) {
+                    constexpr int v = u + kWindow - C::kLoads;   // the next chunk's piece v
+                    pf[v] = __builtin_amdgcn_raw_buffer_load_b128(psrcn, (uint32_t)(16 * lane + 1024 * v), 0,
+                                                                  kNonTemporal);
+                }
+            } else if constexpr (kDirect) {
+                wait_vm<later>();                          // piece u has landed
                 if constexpr (u + kWindow < C::kLoads) dma_piece(std::integral_constant<int, u + kWindow>());
             } else {
+                wait_vm<later>();
                 if constexpr (u + kWindow < C::kLoads) load_piece(u + kWindow);
                 if constexpr (RING) {
                     lds_store4(st + 1024 * (u & 3) + 16 * lane, (u32x4)pf[u]);
@@ -725,16 +790,43 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
         else if (rank == 2) __builtin_amdgcn_s_setprio(2);
         else if (rank >= 3) __builtin_amdgcn_s_setprio(3);
     }
-    stage_chunk(0);
-    decode_chunk();
-    if constexpr (MULTI) {
-        for (int c0 = CH; c0 < nlt; c0 += CH) {
-            const int quarter = 4 * c0 / nlt;              // wave-uniform
-            if (quarter == 1) __builtin_amdgcn_s_setprio(2);
-            else if (quarter == 2) __builtin_amdgcn_s_setprio(1);
-            else if (quarter >= 3) __builtin_amdgcn_s_setprio(0);
-            stage_chunk(c0);
-            decode_chunk();
+    auto chunk_prio = [&](int c0) {
+        const int quarter = 4 * c0 / nlt;                  // wave-uniform
+        if (quarter == 1) __builtin_amdgcn_s_setprio(2);
+        else if (quarter == 2) __builtin_amdgcn_s_setprio(1);
+        else if (quarter >= 3) __builtin_amdgcn_s_setprio(0);
+    };
+    using Yes = std::integral_constant<bool, true>;
+    using No = std::integral_constant<bool, false>;
+    if constexpr (kPipe) {
+        // Whether another chunk follows is known to every chunk's code, so
+        // that the requests, and the waits the compiler puts before their
+        // uses, form one straight sequence per chunk.
+        if (nlt > CH) {
+            stage_pipe(0, Yes(), Yes());
+            decode_chunk(0, Yes());
+            int c0 = CH;
+            for (; nlt - c0 > CH; c0 += CH) {
+                chunk_prio(c0);
+                stage_pipe(c0, Yes(), No());
+                decode_chunk(c0, Yes());
+            }
+            chunk_prio(c0);
+            stage_pipe(c0, No(), No());
+            decode_chunk(c0, No());
+        } else {
+            stage_pipe(0, No(), Yes());
+            decode_chunk(0, No());
+        }
+    } else {
+        stage_chunk(0);
+        decode_chunk(0, No());
+        if constexpr (MULTI) {
+            for (int c0 = CH; c0 < nlt; c0 += CH) {
+                chunk_prio(c0);
+                stage_chunk(c0);
+                decode_chunk(c0, No());
+            }
         }
     }
 
