@@ -192,6 +192,21 @@ def spmm_bench(torch, args, w, N, timer, reorder=False, bits=4):
         if st:
             status[0] = st
 
+    # Setup: every rotating copy is run once and must give copy 0's Y, so a
+    # bad copy cannot go unnoticed. This also has the GPU map each copy's
+    # pages before the timed calls, as the weights of a serving loop are
+    # (each timed call still reads its copy from HBM: the copies together
+    # are far larger than the last-level cache).
+    launch(0)
+    y0 = y.clone()
+    for i in range(1, n_copies):
+        launch(i)
+        if not torch.equal(y, y0):
+            raise RuntimeError(f"rotating copy {i} gives a different Y")
+    torch.cuda.synchronize()
+    if status[0]:
+        raise binding.UsError("us_spmm", status[0])
+
     timer.run(launch, args.warmup)
     torch.cuda.synchronize()
     ms = timer.run(launch, args.steps)
