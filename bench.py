@@ -355,8 +355,14 @@ def main():
         extras["dense_int8_gemm_us"] = round(g_ms * 1e3, 3)
         extras["dense_int8_gemm_gbs"] = round(g_bytes / (g_ms * 1e-3) / 1e9, 1)
         extras["speedup_vs_dense_int8"] = round(g_ms / ms_step, 3)
+        # The floor of any dense INT8 kernel of this shape: the fastest plain
+        # read of its bytes (weights, activations, Y), same rotation.
+        d_ms, _ = read_ceiling(torch, g_bytes, min(args.steps, 1000), timer)
+        extras["dense_int8_read_floor_us"] = round(d_ms * 1e3, 3)
+        extras["speedup_vs_dense_int8_read_floor"] = round(d_ms / ms_step, 3)
         log(f"[bench] read ceiling {extras['read_ceiling_us']} us ({extras['read_ceiling_gbs']} GB/s); "
-            f"dense int8 GEMM {extras['dense_int8_gemm_us']} us")
+            f"dense int8 GEMM {extras['dense_int8_gemm_us']} us; plain read of the dense bytes "
+            f"{extras['dense_int8_read_floor_us']} us")
 
     cpu = None
     if not args.no_cpu:
