@@ -198,13 +198,14 @@ struct SpmmArgs {
 // multi-chunk slices also hold the next chunk's inputs, more of them for
 // longer chunks and wider activation tiles (and, for reordered LTs, their
 // permutation words), and ring staging, like every kernel above 16
-// activation columns, holds the payload pieces in flight in registers.
+// activation columns and the pipelined 16-column kernels of 11- and 16-LT
+// chunks, holds the payload pieces in flight in registers.
 constexpr int waves_per_simd(int wpg, int nmax, int ch, bool multi, bool ring, bool perm) {
     return nmax > 16   ? (multi ? 4 : wpg >= 4 ? 7 : 6)
            : !multi    ? (wpg >= 4 ? 8 : 6)
            : ring      ? (nmax <= 4 ? 5 : 4)
            : nmax <= 4 ? (perm && ch > 11 ? 6 : 7)
-                       : (ch <= 4 ? 7 : ch <= 11 ? 5 : 4);
+                       : (ch <= 4 ? 7 : ch <= 8 || (perm && ch <= 11) ? 5 : 4);
 }
 
 // The launch bound itself: waves_per_simd, except for the kernels above 16
@@ -377,15 +378,17 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     SpmmArgs p, int stage_bytes) {
     constexpr int NB = NMAX > 16 ? 2 : 1;                 // MFMA column blocks
     using C = Chunk<CH, RING, PERM, BITS>;
-    // Pipelined chunks: slices of several chunks whose payload passes through
-    // registers into linear staging (the kernels above 16 activation columns)
-    // request the first pieces of their next chunk while the current chunk's
-    // last pieces are decoded, so that a slice's payload streams without a
-    // round trip at every chunk boundary. Their loads are all visible to the
-    // compiler, whose own waits then order every use exactly. (Not for
-    // reordered 8-LT chunks: the next chunk's pieces would not fit their
-    // register budget.)
-    constexpr bool kPipe = MULTI && !RING && NMAX > 16 && !(PERM && CH > 4);
+    // Pipelined chunks: slices of several chunks in linear staging request
+    // the first pieces of their next chunk while the current chunk's last
+    // pieces are decoded, so that a slice's payload streams without a round
+    // trip at every chunk boundary. Their payload passes through registers
+    // (the next chunk's early pieces wait there until its stage is free), and
+    // their loads are all visible to the compiler, whose own waits then order
+    // every use exactly. This holds above 16 activation columns, and at 16
+    // for chunks of 11 or 16 LTs, whose stage already leaves one workgroup
+    // per CU; not for reordered chunks longer than 4 LTs, whose registers
+    // would not fit the early pieces.
+    constexpr bool kPipe = MULTI && !RING && (NMAX > 16 || (NMAX == 16 && CH >= 11)) && !(PERM && CH > 4);
     static_assert(!kPipe || C::kLoads >= kWindow, "a pipelined chunk takes at least one window of pieces");
     static_assert(BITS == 4 || BITS == 2, "payload values are 4 or 2 bits");
     static_assert(!PERM || BITS == 4, "16-bit row bases hold stage-relative byte slots (4-bit values)");
@@ -498,7 +501,7 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     };
     [[maybe_unused]] uint32_t A0n = 0;                     // (kPipe) the next chunk's first staged byte
     [[maybe_unused]] __amdgpu_buffer_rsrc_t psrcn;         // (kPipe) and its payload range
-    constexpr bool kDirect = !RING && NMAX <= 16;         // payload straight into LDS
+    constexpr bool kDirect = !RING && NMAX <= 16 && !kPipe;  // payload straight into LDS
     auto dma_piece = [&](auto uc) {
         constexpr int u = decltype(uc)::value;
         if (u + 1 < C::kLoads || C::kPayPieces % 64 == 0 || lane + 64 * u < C::kPayPieces)

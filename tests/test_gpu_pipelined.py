@@ -1,14 +1,16 @@
-"""Pipelined chunks (slices of several chunks above 16 activation columns),
-forced, against the oracle.
+"""Pipelined chunks, forced, against the oracle.
 
-Above 16 columns a slice of several chunks requests the first payload pieces
-of its next chunk during the current chunk's last steps. The kernel has
-separate code for the first chunk, the chunks in between and the last one,
-so these cases cover slices of exactly two chunks (no middle chunk), two
-chunks with a one-LT tail, and five chunks, at N = 17 (one column past the
-narrower kernels) and N = 32, for every weight form. The row block's K range
-is one LT short of an equal split, so the wavefronts of a workgroup hold
-slices of different lengths (and, for some, a different number of chunks).
+Above 16 activation columns, and at up to 16 with chunks of 11 or 16 LTs, a
+slice of several chunks requests the first payload pieces of its next chunk
+during the current chunk's last steps. The kernel has separate code for the
+first chunk, the chunks in between and the last one, so these cases cover
+slices of exactly two chunks (no middle chunk), two chunks with a one-LT
+tail, and five chunks, at N = 17 (one column past the 16-column kernels) and
+N = 32 with 4- and 8-LT chunks, and at N = 12 and 16 with 11- and 16-LT
+chunks, for every weight form (reordered chunks longer than 4 LTs keep the
+unpipelined order and are covered too). The row block's K range is one LT
+short of an equal split, so the wavefronts of a workgroup hold slices of
+different lengths (and, for some, a different number of chunks).
 """
 import pytest
 
@@ -21,11 +23,12 @@ pytestmark = pytest.mark.gpu
 def _cases():
     out = []
     for family in ("plain", "reordered", "w2"):
-        for N in (17, 32):
-            for ch in (4, 8):
-                for nlt in (ch + 1, 2 * ch, 5 * ch):
-                    for split in (1, 4):
-                        out.append((family, N, ch, nlt, split))
+        for Ns, chs in (((17, 32), (4, 8)), ((12, 16), (11, 16))):
+            for N in Ns:
+                for ch in chs:
+                    for nlt in (ch + 1, 2 * ch, 5 * ch):
+                        for split in (1, 4):
+                            out.append((family, N, ch, nlt, split))
     return out
 
 

@@ -37,7 +37,7 @@ def waves_per_simd(wpg, nmax, ch, multi, ring, perm):
         return 5 if nmax <= 4 else 4
     if nmax <= 4:
         return 6 if perm and ch > 11 else 7
-    return 7 if ch <= 4 else 5 if ch <= 11 else 4
+    return 7 if ch <= 4 else 5 if ch <= 8 or (perm and ch <= 11) else 4
 
 
 @pytest.fixture(scope="module")
