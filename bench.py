@@ -40,7 +40,8 @@ ROUND_LAUNCHES = 200
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_09291_amd", "csrc", f)
                for f in ("us_spmm_kernel.h", "us_range.h", "us_spmm.hip", "us_spmm_narrow.hip", "us_spmm_perm.hip",
                          "us_spmm_w2.hip", "us_spmm_burst.h", "us_spmm_burst_plain.hip",
-                         "us_spmm_burst_narrow.hip", "us_spmm_burst_perm.hip", "us_spmm_burst_w2.hip")]
+                         "us_spmm_burst_narrow.hip", "us_spmm_burst_perm.hip", "us_spmm_burst_w2.hip")] + [
+    os.path.join(ROOT, "paper_2608_09291_amd", "build.py")]      # its compiler flags shape the kernels too
 
 # HBM traffic of one SpMM launch, read from rocprofv3 --pmc runs of this
 # script (one pass for FETCH_SIZE, one for WRITE_SIZE; KiB per dispatch), each

@@ -3,8 +3,8 @@
     python -m paper_2608_09291_amd.build
 
 compiles ``csrc/*.hip`` with hipcc (gfx950 only, packed FP32 instructions
-disabled) and ``csrc/*.cpp`` with g++, and links ``libunionsparse.so`` next to
-this file.
+disabled, kernel arguments preloaded into scalar registers) and
+``csrc/*.cpp`` with g++, and links ``libunionsparse.so`` next to this file.
 """
 from __future__ import annotations
 
@@ -23,8 +23,12 @@ LIB = os.path.join(PKG, "libunionsparse.so")
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+# Kernel-argument preloading: the leading argument dwords of every kernel
+# arrive in scalar registers at wavefront start (the SpMM kernel orders its
+# arguments for it).
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-fno-strict-aliasing",
-             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-I", INCLUDE]
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-kernarg-preload-count=16",
+             "-I", INCLUDE]
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-fno-strict-aliasing", "-Wall", "-I", INCLUDE]
 
 

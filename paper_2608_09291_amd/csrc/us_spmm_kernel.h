@@ -373,9 +373,33 @@ __device__ __forceinline__ i32x4 unpack_x(uint2 x) {
 // waves_per_simd() resident wavefronts per SIMD (at most 512 / that many
 // VGPRs; held there by its launch bound, see launch_waves), which is also
 // what the host's residency model assumes.
+//
+// The arguments are SpmmArgs field by field, in the order the kernel's first
+// loads need them: the library is built with kernel-argument preloading
+// (the dispatch places the leading argument dwords in scalar registers
+// before the wavefront starts, which gfx950 supports for scalar arguments,
+// not for a structure passed by value). The first loads then wait for no
+// argument fetch; 14 dwords are preloaded, through `scale`.
 template <int WPG, int NMAX, int CH, bool MULTI, bool RING, bool PERM, int BITS>
 __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, PERM)) void us_spmm_kernel(
-    SpmmArgs p, int stage_bytes) {
+    const uint32_t *off, const uint32_t *bm32, const uint8_t *x, int32_t nkb_, int32_t n_, int32_t k_,
+    int32_t pay_bytes, const uint8_t *pay, const float *scale, int32_t n_cu, int stage_bytes, int32_t *y, float *yf,
+    const uint32_t *perm32, int32_t m_) {
+    SpmmArgs p;
+    p.off = off;
+    p.bm32 = bm32;
+    p.x = x;
+    p.nkb = nkb_;
+    p.N = n_;
+    p.K = k_;
+    p.pay_bytes = pay_bytes;
+    p.pay = pay;
+    p.scale = scale;
+    p.n_cu = n_cu;
+    p.y = y;
+    p.yf = yf;
+    p.perm32 = perm32;
+    p.M = m_;
     constexpr int NB = NMAX > 16 ? 2 : 1;                 // MFMA column blocks
     using C = Chunk<CH, RING, PERM, BITS>;
     // Pipelined chunks: slices of several chunks in linear staging request
@@ -909,7 +933,8 @@ hipError_t launch_spmm(const SpmmArgs &a, hipStream_t s) {
         attr_set.fetch_or(bit, std::memory_order_release);
     }
     const int st = stage_bytes<CH, RING, PERM, BITS>(a.N);
-    hipLaunchKernelGGL(kern, dim3(a.M / 16), dim3(64 * WPG), WPG * st, s, a, st);
+    hipLaunchKernelGGL(kern, dim3(a.M / 16), dim3(64 * WPG), WPG * st, s, a.off, a.bm32, a.x, a.nkb, a.N, a.K,
+                       a.pay_bytes, a.pay, a.scale, a.n_cu, st, a.y, a.yf, a.perm32, a.M);
     return hipGetLastError();
 }
 

@@ -8,7 +8,10 @@ wavefronts (512 per SIMD lane, in granules of 8; the kernels use no AGPRs,
 so the VGPR count is the whole register budget) and that it needs no
 scratch. The expected figures restate the kernel header's waves_per_simd
 table. Kernels above 16 activation columns on rows in stored order carry no
-launch bound, so their budget is the four wavefronts the table assumes.
+launch bound, so their budget is the four wavefronts the table assumes. The
+units are compiled with the library's flags, kernel-argument preloading
+included, and every SpMM kernel is checked to take its leading arguments
+preloaded.
 """
 import concurrent.futures as cf
 import os
@@ -24,7 +27,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 UNITS = ("us_dense", "us_spmm", "us_spmm_narrow", "us_spmm_perm", "us_spmm_w2", "us_spmm_burst_plain", "us_spmm_burst_narrow",
          "us_spmm_burst_perm", "us_spmm_burst_w2")
 FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fno-strict-aliasing", "-Xclang", "-target-feature",
-         "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"), "-I", CSRC, "--cuda-device-only", "-S"]
+         "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-kernarg-preload-count=16", "-I", os.path.join(ROOT, "include"),
+         "-I", CSRC, "--cuda-device-only", "-S"]
 
 
 
@@ -78,8 +82,9 @@ def kernels():
             wpg, nmax, ch, multi, ring, perm, bits = (int(v) for v in g.groups())
             vgpr = int(re.search(r"\.amdhsa_next_free_vgpr (\d+)", m.group(2)).group(1))
             scratch = int(re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", m.group(2)).group(1))
+            preload = int(re.search(r"\.amdhsa_user_sgpr_kernarg_preload_length (\d+)", m.group(2)).group(1))
             found.append(dict(wpg=wpg, nmax=nmax, ch=ch, multi=bool(multi), ring=bool(ring), perm=bool(perm),
-                              bits=bits, vgpr=vgpr, scratch=scratch))
+                              bits=bits, vgpr=vgpr, scratch=scratch, preload=preload))
     return found, m0_lines, burst
 
 
@@ -135,3 +140,11 @@ def test_registers_fit_the_residency_the_host_assumes(kernel_list):
 def test_no_kernel_needs_scratch(kernel_list):
     spills = [k for k in kernel_list if k["scratch"]]
     assert not spills, spills[:5]
+
+
+def test_leading_arguments_are_preloaded(kernel_list):
+    # Built as the library is, every SpMM kernel takes its first 14 argument
+    # dwords (the inputs' addresses and sizes its first loads need, through
+    # the scale pointer) preloaded in scalar registers.
+    short = [k for k in kernel_list if k["preload"] < 14]
+    assert not short, short[:5]
