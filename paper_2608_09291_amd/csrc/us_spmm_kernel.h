@@ -265,6 +265,13 @@ __device__ __forceinline__ void dma16(u32x4 desc, uint32_t lds, uint32_t voff, u
 }
 #pragma clang diagnostic pop
 
+// (q MAGIC) >> SHIFT equals q / P for every 0 <= q < qend.
+constexpr bool row_by_multiply(int P, uint32_t magic, int shift, int qend) {
+    for (int q = 0; q < qend; ++q)
+        if ((((uint32_t)q * magic) >> shift) != (uint32_t)(q / P)) return false;
+    return true;
+}
+
 // f(std::integral_constant<int, U>) for U = B .. E-1, as straight-line code.
 template <int B, int E, typename F>
 __device__ __forceinline__ void static_for(F &&f) {
@@ -460,19 +467,41 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     const __amdgpu_buffer_rsrc_t xsrc =
         __builtin_amdgcn_make_buffer_rsrc((void *)p.x, (short)0, N * xrow_bytes, kBufferDword3);
     // Activation staging: the chunk's N x 2 CH pieces of 16 bytes, piece
-    // q = lane + 64 u is row q / (2 CH), piece q % (2 CH). Only the loads
-    // that carry pieces are issued (all of them in pipelined slices, whose
+    // q = lane + 64 u in load u. Only the loads that carry pieces are issued (all of them in pipelined slices, whose
     // wait counts must not depend on N: the others read zero, with no
     // memory traffic): the texture path, not HBM, limits how fast a CU takes
     // them in at the start of the kernel.
     constexpr int kXLoads = (NMAX * C::kXPieces + 63) / 64;
     const int x_loads = (N * C::kXPieces + 63) / 64;                           // wave-uniform
-    uint32_t xv[kXLoads], xs[kXLoads];                     // global byte offset, LDS address
+    // Piece q is row n = q / (2 CH), piece q - 2 CH n of it; rows >= N read
+    // zero. With 2 CH a power of two that is a shift. Otherwise (11-LT
+    // chunks) n comes from a multiply and a shift (exact for every q the
+    // loads reach), and the piece's offsets follow from n and q without a
+    // division: in the slice n K/2 + 16 (q - 2 CH n) bytes, in LDS st_x +
+    // 16 (q + n), as a staged row holds 16 bytes more than its 2 CH pieces.
+    // This address arithmetic runs before the loads can be issued, on every
+    // wavefront of the CU at once.
+    constexpr bool kXPow2 = (C::kXPieces & (C::kXPieces - 1)) == 0;
+    constexpr int kXShift = 20;
+    constexpr uint32_t kXMagic = ((1u << kXShift) + C::kXPieces - 1) / C::kXPieces;
+    static_assert(row_by_multiply(C::kXPieces, kXMagic, kXShift, 64 * kXLoads), "inexact activation row");
+    auto x_piece = [&](int u) { return (uint32_t)(lane + 64 * u); };
+    auto x_row = [&](int u) { return (x_piece(u) * kXMagic) >> kXShift; };
+    const int x_step = xrow_bytes - 16 * C::kXPieces;      // |x_step| < 2^23
+    // Global byte offsets, and LDS addresses (0: a row >= N) where kept: in
+    // every multi-chunk slice and with a power-of-two row; single-chunk
+    // slices of 11-LT chunks compute them when the pieces are stored.
+    uint32_t xv[kXLoads];
+    [[maybe_unused]] uint32_t xs[kXLoads];
 #pragma unroll
     for (int u = 0; u < kXLoads; ++u) {
-        const int q = lane + 64 * u, n = q / C::kXPieces, pj = q % C::kXPieces;
-        xv[u] = (uint32_t)(n * xrow_bytes + 16 * pj);      // rows >= N fall outside the range: zero
-        xs[u] = n < N ? st_x + 4u * (uint32_t)(n * C::kXRowWords) + 16u * (uint32_t)pj : 0u;
+        if constexpr (kXPow2) {
+            const int q = lane + 64 * u, n = q / C::kXPieces, pj = q % C::kXPieces;
+            xv[u] = (uint32_t)(n * xrow_bytes + 16 * pj);
+            xs[u] = n < N ? st_x + 4u * (uint32_t)(n * C::kXRowWords) + 16u * (uint32_t)pj : 0u;
+        } else {
+            xv[u] = 16u * x_piece(u) + (uint32_t)__mul24((int)x_row(u), x_step);
+        }
     }
 
     i32x4 acc[NB];
@@ -498,6 +527,13 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     };
 
     request(0);
+    if constexpr (MULTI && !kXPow2) {
+#pragma unroll
+        for (int u = 0; u < kXLoads; ++u) {
+            const uint32_t n = x_row(u);
+            xs[u] = n < (uint32_t)N ? st_x + 16u * (x_piece(u) + n) : 0u;
+        }
+    }
     // The dequant scale of the output row this thread stores in the epilogue
     // (outputs e = threadIdx.x + 64 WPG k all have row e mod 16), requested
     // now so that the epilogue does not wait for it.
@@ -544,8 +580,14 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
             if (lane < CH) lds_store2(st_base + 64 * lane, (u32x2){lane_rows(pperm.x), lane_rows(pperm.y)});
         }
 #pragma unroll
-        for (int u = 0; u < kXLoads; ++u)
-            if (u < x_loads && xs[u] != 0u) lds_store4(xs[u], (u32x4)px[u]);
+        for (int u = 0; u < kXLoads; ++u) {
+            if constexpr (MULTI || kXPow2) {
+                if (u < x_loads && xs[u] != 0u) lds_store4(xs[u], (u32x4)px[u]);
+            } else {
+                const uint32_t n = x_row(u);
+                if (u < x_loads && n < (uint32_t)N) lds_store4(st_x + 16u * (x_piece(u) + n), (u32x4)px[u]);
+            }
+        }
     };
     // (kPipe) Stage a chunk of a pipelined slice; NX: another chunk follows.
     // The first chunk requests its first pieces here; a later chunk's were
