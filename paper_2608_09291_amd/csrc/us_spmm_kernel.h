@@ -436,11 +436,17 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     // This wavefront's K slice: LTs t0 .. t0 + nlt - 1 of row block mb
     // (nlt >= 1 because WPG <= K / 64). When the LTs do not divide evenly,
     // the first K/64 mod WPG wavefronts take one more; the last ones, which
-    // the SIMDs serve last, are the short slices.
+    // the SIMDs serve last, are the short slices. (Unsigned arithmetic: the
+    // scalar instructions before the first loads are few, as every
+    // wavefront of a CU issues them at once.)
     const int nkb = p.nkb;
-    const int kb0 = wave * (nkb / WPG) + min(wave, nkb % WPG);
-    const int nlt = nkb / WPG + (wave < nkb % WPG ? 1 : 0);
-    const int64_t t0 = (int64_t)mb * nkb + kb0;
+    const uint32_t unkb = (uint32_t)nkb;
+    const int kb0 = (int)((uint32_t)wave * (unkb / WPG) + min((uint32_t)wave, unkb % WPG));
+    const int nlt = (int)(unkb / WPG + ((uint32_t)wave < unkb % WPG ? 1u : 0u));
+    const uint64_t t0 = (uint64_t)(uint32_t)mb * unkb + (uint32_t)kb0;
+    const uint32_t *const off_s = p.off + t0;              // the slice's offsets, bitmaps, permutations
+    const uint32_t *const bm_s = p.bm32 + 8 * t0;
+    [[maybe_unused]] const uint32_t *const perm_s = p.perm32 + 2 * t0;
 
     // Lane roles in the decode.
     const int rr = lane & 15;
@@ -463,7 +469,7 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     for (int nb = 0; nb < NB; ++nb) xq[nb] = st_x + 4u * (uint32_t)(min(nb * 16 + rr, N - 1) * C::kXRowWords + g);
 
     // Activation loads: whole rows of K/2 bytes; rows >= N read zero.
-    const int xrow_bytes = p.K / 2;
+    const int xrow_bytes = (int)((uint32_t)p.K >> 1);
     const __amdgpu_buffer_rsrc_t xsrc =
         __builtin_amdgcn_make_buffer_rsrc((void *)p.x, (short)0, N * xrow_bytes, kBufferDword3);
     // Activation staging: the chunk's N x 2 CH pieces of 16 bytes, piece
@@ -472,7 +478,7 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     // memory traffic): the texture path, not HBM, limits how fast a CU takes
     // them in at the start of the kernel.
     constexpr int kXLoads = (NMAX * C::kXPieces + 63) / 64;
-    const int x_loads = (N * C::kXPieces + 63) / 64;                           // wave-uniform
+    const int x_loads = (int)(((uint32_t)N * C::kXPieces + 63u) >> 6);        // wave-uniform
     // Piece q is row n = q / (2 CH), piece q - 2 CH n of it; rows >= N read
     // zero. With 2 CH a power of two that is a shift. Otherwise (11-LT
     // chunks) n comes from a multiply and a shift (exact for every q the
@@ -517,9 +523,9 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     i32x4 px[kXLoads];
     auto request = [&](int c0) {
         const int cnt = min(CH, nlt - c0);                 // >= 1
-        offv = p.off[t0 + c0 + min(lane, cnt)];
-        pbm = *(const u32x4 *)(p.bm32 + 8 * (t0 + c0) + 4 * min(lane, 2 * cnt - 1));
-        if constexpr (PERM) pperm = *(const u32x2 *)(p.perm32 + 2 * (t0 + c0 + min(lane, cnt - 1)));
+        offv = off_s[(uint32_t)(c0 + min(lane, cnt))];
+        pbm = *(const u32x4 *)(bm_s + (uint32_t)(8 * c0 + 4 * min(lane, 2 * cnt - 1)));
+        if constexpr (PERM) pperm = *(const u32x2 *)(perm_s + (uint32_t)(2 * (c0 + min(lane, cnt - 1))));
         const uint32_t xk = (uint32_t)(32 * (kb0 + c0));
 #pragma unroll
         for (int u = 0; u < kXLoads; ++u)
