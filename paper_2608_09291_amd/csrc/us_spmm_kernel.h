@@ -444,9 +444,8 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     const int kb0 = (int)((uint32_t)wave * (unkb / WPG) + min((uint32_t)wave, unkb % WPG));
     const int nlt = (int)(unkb / WPG + ((uint32_t)wave < unkb % WPG ? 1u : 0u));
     const uint64_t t0 = (uint64_t)(uint32_t)mb * unkb + (uint32_t)kb0;
-    const uint32_t *const off_s = p.off + t0;              // the slice's offsets, bitmaps, permutations
-    const uint32_t *const bm_s = p.bm32 + 8 * t0;
-    [[maybe_unused]] const uint32_t *const perm_s = p.perm32 + 2 * t0;
+    [[maybe_unused]] const uint32_t *const off_s = p.off + t0;   // the slice's offsets and bitmaps
+    [[maybe_unused]] const uint32_t *const bm_s = p.bm32 + 8 * t0;
 
     // Lane roles in the decode.
     const int rr = lane & 15;
@@ -523,9 +522,16 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
     i32x4 px[kXLoads];
     auto request = [&](int c0) {
         const int cnt = min(CH, nlt - c0);                 // >= 1
-        offv = off_s[(uint32_t)(c0 + min(lane, cnt))];
-        pbm = *(const u32x4 *)(bm_s + (uint32_t)(8 * c0 + 4 * min(lane, 2 * cnt - 1)));
-        if constexpr (PERM) pperm = *(const u32x2 *)(perm_s + (uint32_t)(2 * (c0 + min(lane, cnt - 1))));
+        if constexpr (!PERM) {
+            offv = off_s[(uint32_t)(c0 + min(lane, cnt))];
+            pbm = *(const u32x4 *)(bm_s + (uint32_t)(8 * c0 + 4 * min(lane, 2 * cnt - 1)));
+        } else {
+            // (64-bit lane addresses: scalar bases would leave the reordered
+            // multi-chunk kernels above 16 columns short of registers)
+            offv = p.off[t0 + c0 + min(lane, cnt)];
+            pbm = *(const u32x4 *)(p.bm32 + 8 * (t0 + c0) + 4 * min(lane, 2 * cnt - 1));
+            pperm = *(const u32x2 *)(p.perm32 + 2 * (t0 + c0 + min(lane, cnt - 1)));
+        }
         const uint32_t xk = (uint32_t)(32 * (kb0 + c0));
 #pragma unroll
         for (int u = 0; u < kXLoads; ++u)
