@@ -591,13 +591,21 @@ __global__ __launch_bounds__(64 * WPG, launch_waves(WPG, NMAX, CH, MULTI, RING, 
             auto lane_rows = [](uint32_t w) { return ((w << 1) & 0xEEEEEEEEu) | ((w >> 3) & 0x11111111u); };
             if (lane < CH) lds_store2(st_base + 64 * lane, (u32x2){lane_rows(pperm.x), lane_rows(pperm.y)});
         }
+        // Loads past x_loads were not issued. The reordered and 2-bit
+        // single-chunk kernels for up to 16 columns branch past their
+        // stores on that wave-uniform count (4-5 % faster on 4096x11008 at
+        // N = 8, 2 % on 12288x4096); the plain 4-bit, the multi-chunk and
+        // the 4-column kernels measured 1-2 % slower with the branch and
+        // mask the stores lane by lane instead.
+        constexpr bool kXBranch = (PERM || BITS == 2) && !MULTI && NMAX == 16;
 #pragma unroll
         for (int u = 0; u < kXLoads; ++u) {
+            if (kXBranch && u >= x_loads) break;
             if constexpr (MULTI || kXPow2) {
-                if (u < x_loads && xs[u] != 0u) lds_store4(xs[u], (u32x4)px[u]);
+                if ((kXBranch || u < x_loads) && xs[u] != 0u) lds_store4(xs[u], (u32x4)px[u]);
             } else {
                 const uint32_t n = x_row(u);
-                if (u < x_loads && n < (uint32_t)N) lds_store4(st_x + 16u * (x_piece(u) + n), (u32x4)px[u]);
+                if ((kXBranch || u < x_loads) && n < (uint32_t)N) lds_store4(st_x + 16u * (x_piece(u) + n), (u32x4)px[u]);
             }
         }
     };
