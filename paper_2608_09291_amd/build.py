@@ -3,7 +3,8 @@
     python -m paper_2608_09291_amd.build
 
 compiles ``csrc/*.hip`` with hipcc (gfx950 only, packed FP32 instructions
-disabled, kernel arguments preloaded into scalar registers) and
+disabled, kernel arguments preloaded into scalar registers, iterative ILP
+scheduling) and
 ``csrc/*.cpp`` with g++, and links ``libunionsparse.so`` next to this file.
 """
 from __future__ import annotations
@@ -29,6 +30,17 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-fno-strict-aliasing",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-kernarg-preload-count=16",
              "-I", INCLUDE]
+# The iterative ILP scheduling strategy measured 0-3 % faster than the
+# default on the SpMM workloads up to 16 activation columns; the kernels
+# above 16 columns (us_spmm_wide.hip) keep the default, with which they fit
+# the registers of four wavefronts per SIMD.
+DEFAULT_SCHED_UNITS = ("us_spmm_wide.hip",)
+
+
+def hip_flags(source: str) -> list:
+    """hipcc flags for one csrc/*.hip file (without -c/-o)."""
+    sched = [] if source in DEFAULT_SCHED_UNITS else ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]
+    return HIP_FLAGS + sched
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-fno-strict-aliasing", "-Wall", "-I", INCLUDE]
 
 
@@ -52,7 +64,7 @@ def build(verbose: bool = False) -> str:
     jobs = []
     for f in hip:
         obj = os.path.join(BUILD, f + ".o")
-        jobs.append((obj, [HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, f), "-o", obj]))
+        jobs.append((obj, [HIPCC, *hip_flags(f), "-c", os.path.join(CSRC, f), "-o", obj]))
     for f in cpp:
         obj = os.path.join(BUILD, f + ".o")
         jobs.append((obj, ["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, f), "-o", obj]))

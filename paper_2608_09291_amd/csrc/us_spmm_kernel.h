@@ -1013,12 +1013,17 @@ hipError_t launch_spmm_wpg(int wpg, const SpmmArgs &a, hipStream_t s) {
 
 // Launch configuration idx of kCfgs with wpg wavefronts per workgroup, for
 // N <= 16 (NMAX = 4 or 16) or N <= 32.
+// The instantiations above 16 activation columns (NMAX = 32) of every weight
+// form live in a translation unit of their own, built with the compiler's
+// default scheduling strategy: the one the others use leaves some of them
+// above the registers of four wavefronts per SIMD.
+template <bool PERM, int BITS>
+hipError_t launch_cfg_wide(int wpg, int idx, const SpmmArgs &a, hipStream_t s);
+
 template <bool PERM, int BITS, int NMAX = 16>
 hipError_t launch_cfg(int wpg, int idx, const SpmmArgs &a, hipStream_t s) {
     if constexpr (NMAX > 4) {
-        if (a.N > 16)
-            return idx == 1 ? launch_spmm_wpg<32, 8, false, PERM, BITS>(wpg, a, s)
-                            : launch_spmm_wpg<32, 4, false, PERM, BITS>(wpg, a, s);
+        if (a.N > 16) return launch_cfg_wide<PERM, BITS>(wpg, idx, a, s);
     }
     switch (idx) {
         case 5: return launch_spmm_wpg<NMAX, 11, true, PERM, BITS>(wpg, a, s);

@@ -21,14 +21,18 @@ import tempfile
 
 import pytest
 
+from paper_2608_09291_amd import build
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2608_09291_amd", "csrc")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-UNITS = ("us_dense", "us_spmm", "us_spmm_narrow", "us_spmm_perm", "us_spmm_w2", "us_spmm_burst_plain", "us_spmm_burst_narrow",
-         "us_spmm_burst_perm", "us_spmm_burst_w2")
-FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fno-strict-aliasing", "-Xclang", "-target-feature",
-         "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-kernarg-preload-count=16", "-I", os.path.join(ROOT, "include"),
-         "-I", CSRC, "--cuda-device-only", "-S"]
+UNITS = ("us_dense", "us_spmm", "us_spmm_narrow", "us_spmm_perm", "us_spmm_w2", "us_spmm_wide", "us_spmm_burst_plain",
+         "us_spmm_burst_narrow", "us_spmm_burst_perm", "us_spmm_burst_w2")
+
+
+def unit_flags(unit):
+    # The library's own flags for the unit (build.py), device code only, as assembly.
+    return [f for f in build.hip_flags(unit + ".hip") if f != "-fPIC"] + ["-I", CSRC, "--cuda-device-only", "-S"]
 
 
 
@@ -52,7 +56,8 @@ def kernels():
 
     def compile_unit(u):
         out = os.path.join(tmp, u + ".s")
-        r = subprocess.run([HIPCC, *FLAGS, os.path.join(CSRC, u + ".hip"), "-o", out], capture_output=True, text=True)
+        r = subprocess.run([HIPCC, *unit_flags(u), os.path.join(CSRC, u + ".hip"), "-o", out], capture_output=True,
+                           text=True)
         assert r.returncode == 0, r.stderr[-2000:]
         return open(out).read()
 
