@@ -1015,8 +1015,8 @@ hipError_t launch_spmm_wpg(int wpg, const SpmmArgs &a, hipStream_t s) {
 // N <= 16 (NMAX = 4 or 16) or N <= 32.
 // The instantiations above 16 activation columns (NMAX = 32) of every weight
 // form live in a translation unit of their own, built with the compiler's
-// default scheduling strategy: the one the others use leaves some of them
-// above the registers of four wavefronts per SIMD.
+// default scheduling strategy: the one the plain and 2-bit units use leaves
+// some of them above the registers of four wavefronts per SIMD.
 template <bool PERM, int BITS>
 hipError_t launch_cfg_wide(int wpg, int idx, const SpmmArgs &a, hipStream_t s);
 

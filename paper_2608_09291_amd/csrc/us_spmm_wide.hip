@@ -2,8 +2,8 @@
 // two MFMA column blocks) for every weight form: 4-bit rows in stored
 // order, row-reordered 4-bit, and 2-bit. A translation unit of its own, as
 // the library builds it with the compiler's default scheduling strategy
-// (the others use the iterative ILP strategy, which leaves some of these
-// kernels above the registers of four wavefronts per SIMD).
+// (the plain and 2-bit units use the iterative ILP strategy, which leaves
+// some of these kernels above the registers of four wavefronts per SIMD).
 #include "us_spmm_kernel.h"
 
 namespace us_spmm_detail {
