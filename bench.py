@@ -39,7 +39,7 @@ ROTATE_BYTES = 1 << 30
 ROUND_LAUNCHES = 200
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_09291_amd", "csrc", f)
                for f in ("us_spmm_kernel.h", "us_range.h", "us_spmm.hip", "us_spmm_narrow.hip", "us_spmm_perm.hip",
-                         "us_spmm_w2.hip", "us_spmm_wide.hip", "us_spmm_burst.h", "us_spmm_burst_plain.hip",
+                         "us_spmm_w2.hip", "us_spmm_wide.hip", "us_spmm_wide8.hip", "us_spmm_burst.h", "us_spmm_burst_plain.hip",
                          "us_spmm_burst_narrow.hip", "us_spmm_burst_perm.hip", "us_spmm_burst_w2.hip")] + [
     os.path.join(ROOT, "paper_2608_09291_amd", "build.py")]      # its compiler flags shape the kernels too
 

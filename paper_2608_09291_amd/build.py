@@ -31,12 +31,12 @@ HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-fno-stric
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-kernarg-preload-count=16",
              "-I", INCLUDE]
 # The iterative ILP scheduling strategy measured 0-3 % faster than the
-# default on the SpMM workloads up to 16 activation columns with rows in
-# stored order, 4- and 2-bit. The kernels above 16 columns (us_spmm_wide.hip)
-# keep the default, with which they fit the registers of four wavefronts per
-# SIMD, and so do the row-reordered ones (us_spmm_perm.hip), which measured
-# 1 % slower with it.
-DEFAULT_SCHED_UNITS = ("us_spmm_wide.hip", "us_spmm_perm.hip")
+# default on the SpMM workloads with rows in stored order, 4- and 2-bit. The
+# kernels above 16 columns with 8-LT chunks (us_spmm_wide8.hip) keep the
+# default, with which they fit the registers of four wavefronts per SIMD,
+# and so do the row-reordered ones up to 16 columns (us_spmm_perm.hip),
+# which measured 1 % slower with it.
+DEFAULT_SCHED_UNITS = ("us_spmm_wide8.hip", "us_spmm_perm.hip")
 
 
 def hip_flags(source: str) -> list:

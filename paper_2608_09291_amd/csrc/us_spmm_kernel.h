@@ -1014,11 +1014,14 @@ hipError_t launch_spmm_wpg(int wpg, const SpmmArgs &a, hipStream_t s) {
 // Launch configuration idx of kCfgs with wpg wavefronts per workgroup, for
 // N <= 16 (NMAX = 4 or 16) or N <= 32.
 // The instantiations above 16 activation columns (NMAX = 32) of every weight
-// form live in a translation unit of their own, built with the compiler's
-// default scheduling strategy: the one the plain and 2-bit units use leaves
-// some of them above the registers of four wavefronts per SIMD.
+// form live in translation units of their own: us_spmm_wide.hip (4-LT
+// chunks) and us_spmm_wide8.hip (8-LT chunks), the latter built with the
+// compiler's default scheduling strategy, as the one the other units use
+// leaves some of its kernels above the registers of four wavefronts per SIMD.
 template <bool PERM, int BITS>
 hipError_t launch_cfg_wide(int wpg, int idx, const SpmmArgs &a, hipStream_t s);
+template <bool PERM, int BITS>
+hipError_t launch_cfg_wide8(int wpg, const SpmmArgs &a, hipStream_t s);
 
 template <bool PERM, int BITS, int NMAX = 16>
 hipError_t launch_cfg(int wpg, int idx, const SpmmArgs &a, hipStream_t s) {

@@ -26,8 +26,8 @@ from paper_2608_09291_amd import build
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2608_09291_amd", "csrc")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-UNITS = ("us_dense", "us_spmm", "us_spmm_narrow", "us_spmm_perm", "us_spmm_w2", "us_spmm_wide", "us_spmm_burst_plain",
-         "us_spmm_burst_narrow", "us_spmm_burst_perm", "us_spmm_burst_w2")
+UNITS = ("us_dense", "us_spmm", "us_spmm_narrow", "us_spmm_perm", "us_spmm_w2", "us_spmm_wide", "us_spmm_wide8",
+         "us_spmm_burst_plain", "us_spmm_burst_narrow", "us_spmm_burst_perm", "us_spmm_burst_w2")
 
 
 def unit_flags(unit):
