@@ -82,9 +82,15 @@ bool burst_from_opts(const us_spmm_opts &o, int nkb, int N, bool perm, int bits,
 // LT decodes; and each LT's decode time grows with the wavefronts sharing a
 // SIMD (v / 4) once there is one per SIMD, as the decode is issue-bound.
 // Ties go to fewer generations, then to more wavefronts per CU, then to
-// linear staging and shorter chunks. The constants were fitted to a sweep of
-// every configuration over 17 shapes and widths: within 0.5 % of the fastest
-// on average, 4 % at worst. Residency: the LDS, and the wavefronts per SIMD
+// linear staging and shorter chunks. Only the kernels of up to 4 columns on
+// rows in stored order, with at least one row block per CU, take fewer
+// wavefronts on a tie: their per-wavefront start outweighs the added
+// parallelism there (12288x4096 at N = 1-4 runs 5-7 % faster as 4 x 16 than
+// as 8 x 8), while with fewer row blocks than CUs (1024x4096: 17 % slower)
+// or reordered rows (28672x8192 at N = 1: 3 % slower) it does not. The constants were
+// fitted to a sweep of every configuration over 17 shapes and widths; a
+// later sweep of 27 shapes and widths puts the choice within 0.7 % of the
+// fastest on average, 7 % at worst. Residency: the LDS, and the wavefronts per SIMD
 // each instantiation is built for (waves_per_simd), with at most 16
 // workgroups per CU.
 // wpg_only > 0 fixes the number of wavefronts; staging 1 or 2 allows linear
@@ -120,7 +126,8 @@ void choose_config(int M, int K, int N, bool perm, int bits, int n_cu, int wpg_o
                 const long v = (long)w * ((min(left, slots) + n_cu - 1) / n_cu);   // busiest CU
                 cost += 40 + chunks * (20 + c * max(4L, v));
             }
-            const long key[5] = {cost, gens, -waves, kCfgs[idx].ring ? 1 : 0, c};
+            const bool fewer = nmax == 4 && !perm && nrb >= n_cu;   // see the tie rule above
+            const long key[5] = {cost, gens, fewer ? waves : -waves, kCfgs[idx].ring ? 1 : 0, c};
             bool better = cfg < 0;
             for (int k = 0; k < 5 && !better; ++k) {
                 if (key[k] != best[k]) {

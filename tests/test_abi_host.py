@@ -284,9 +284,11 @@ def test_pack_int4_layout():
 @pytest.mark.parametrize("M,K,N,plan", [
     (4096, 11008, 8, (16, 11, 1)),     # one generation of 16-wavefront workgroups
     (12288, 4096, 8, (4, 16, 2)),      # the ring lets three workgroups share a CU
-    (28672, 8192, 1, (4, 8, 1)),       # seven workgroups of four per CU (seven per SIMD), four 8-LT chunks
+    (28672, 8192, 1, (2, 16, 1)),      # a cost tie at up to 4 columns goes to fewer wavefronts: 2 x 16
+    (12288, 4096, 1, (4, 16, 1)),      # the same tie: 4 x 16 rather than 8 x 8
     (28672, 7168, 8, (4, 4, 1)),       # 4-LT chunks keep seven wavefronts per SIMD in one generation
-    (12288, 49152, 4, (8, 8, 1)),      # 24 wavefronts per CU beat 12 in a single generation
+    (12288, 49152, 4, (4, 16, 1)),     # the same tie, level in time with 8 x 8
+    (1024, 4096, 1, (16, 4, 1)),       # 64 row blocks for 256 CUs: the tie keeps more wavefronts
     (28672, 8192, 32, (2, 4, 1)),      # two column blocks, 1792 row blocks: two generations would cost more
     (4096, 11008, 32, (16, 4, 1)),     # 256 row blocks: one generation, so 16 slices of three 4-LT chunks
 ])
