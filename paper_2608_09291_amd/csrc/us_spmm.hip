@@ -82,12 +82,15 @@ bool burst_from_opts(const us_spmm_opts &o, int nkb, int N, bool perm, int bits,
 // LT decodes; and each LT's decode time grows with the wavefronts sharing a
 // SIMD (v / 4) once there is one per SIMD, as the decode is issue-bound.
 // Ties go to fewer generations, then to more wavefronts per CU, then to
-// linear staging and shorter chunks. Only the kernels of up to 4 columns on
-// rows in stored order, with at least one row block per CU, take fewer
-// wavefronts on a tie: their per-wavefront start outweighs the added
-// parallelism there (12288x4096 at N = 1-4 runs 5-7 % faster as 4 x 16 than
-// as 8 x 8), while with fewer row blocks than CUs (1024x4096: 17 % slower)
-// or reordered rows (28672x8192 at N = 1: 3 % slower) it does not. The constants were
+// linear staging and shorter chunks. The kernels of up to 4 columns on rows
+// in stored order differ in two ways, both measured: they take a ring stage
+// only when no linear one fits (linear staging was the faster on every
+// shape swept at N <= 4, by up to 7 %), and, with at least one row block
+// per CU, a tie goes to fewer wavefronts as long as 8 or more stay on the
+// CU (their per-wavefront start outweighs the added parallelism there:
+// 12288x4096 at N = 1-4 runs 5-7 % faster as 4 x 16 than as 8 x 8, while
+// one wavefront per slice of 28672x7168, fewer row blocks than CUs
+// (1024x4096) or reordered rows (28672x8192 at N = 1) run 3-23 % slower). The constants were
 // fitted to a sweep of every configuration over 17 shapes and widths; a
 // later sweep of 27 shapes and widths puts the choice within 0.7 % of the
 // fastest on average, 7 % at worst. Residency: the LDS, and the wavefronts per SIMD
@@ -101,7 +104,7 @@ bool burst_from_opts(const us_spmm_opts &o, int nkb, int N, bool perm, int bits,
 void choose_config(int M, int K, int N, bool perm, int bits, int n_cu, int wpg_only, int staging, int ch_only,
                    int &wpg, int &cfg) {
     const int nrb = M / 16, nkb = K / 64;
-    long best[5] = {0, 0, 0, 0, 0};
+    long best[6] = {0, 0, 0, 0, 0, 0};
     wpg = 0;
     cfg = -1;
     // Activation width the instantiation is built for (us_spmm's dispatch).
@@ -126,17 +129,19 @@ void choose_config(int M, int K, int N, bool perm, int bits, int n_cu, int wpg_o
                 const long v = (long)w * ((min(left, slots) + n_cu - 1) / n_cu);   // busiest CU
                 cost += 40 + chunks * (20 + c * max(4L, v));
             }
-            const bool fewer = nmax == 4 && !perm && nrb >= n_cu;   // see the tie rule above
-            const long key[5] = {cost, gens, fewer ? waves : -waves, kCfgs[idx].ring ? 1 : 0, c};
+            const bool narrow = nmax == 4 && !perm;               // see the rules above
+            const long ring_last = narrow && kCfgs[idx].ring ? 1 : 0;
+            const long tie = narrow && nrb >= n_cu ? (waves >= 8 ? waves : 1000000 - waves) : -waves;
+            const long key[6] = {ring_last, cost, gens, tie, kCfgs[idx].ring ? 1 : 0, c};
             bool better = cfg < 0;
-            for (int k = 0; k < 5 && !better; ++k) {
+            for (int k = 0; k < 6 && !better; ++k) {
                 if (key[k] != best[k]) {
                     better = key[k] < best[k];
                     break;
                 }
             }
             if (better) {
-                for (int k = 0; k < 5; ++k) best[k] = key[k];
+                for (int k = 0; k < 6; ++k) best[k] = key[k];
                 wpg = w;
                 cfg = idx;
             }

@@ -289,6 +289,8 @@ def test_pack_int4_layout():
     (28672, 7168, 8, (4, 4, 1)),       # 4-LT chunks keep seven wavefronts per SIMD in one generation
     (12288, 49152, 4, (4, 16, 1)),     # the same tie, level in time with 8 x 8
     (1024, 4096, 1, (16, 4, 1)),       # 64 row blocks for 256 CUs: the tie keeps more wavefronts
+    (28672, 7168, 1, (2, 8, 1)),       # fewer wavefronts on a tie, but at least 8 per CU (not 1 x 16)
+    (28672, 8192, 2, (2, 11, 1)),      # up to 4 columns, a linear stage rather than a ring
     (28672, 8192, 32, (2, 4, 1)),      # two column blocks, 1792 row blocks: two generations would cost more
     (4096, 11008, 32, (16, 4, 1)),     # 256 row blocks: one generation, so 16 slices of three 4-LT chunks
 ])
