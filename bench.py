@@ -56,7 +56,7 @@ KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_09291_amd", "csrc", f)
 # traffic is unknown. Keyed by workload, N and row reordering.
 COPY_FACTOR = {"FETCH_SIZE": 131083.0 / 262144.0, "WRITE_SIZE": 262144.0 / 262144.0}
 MEASURED_TRAFFIC = {
-    ("ffn_down_4096x11008_s50", 8, False): dict(src="28004390cc5be152", FETCH_SIZE=11374.3125, WRITE_SIZE=256.0),
+    ("ffn_down_4096x11008_s50", 8, False): dict(src="18f3c274054a93c2", FETCH_SIZE=11374.3125, WRITE_SIZE=256.0),
 }
 
 
